@@ -1,0 +1,239 @@
+/*
+ * pallas.h -- C ABI of the MI355X (gfx950) library for target-side KV-cache
+ * reconstruction (Pallas, arXiv 2608.16477).
+ *
+ * The method (Section 4.3, "Parallel State Preparation"): at the trigger the
+ * source splits the token sequence at position k; the target rebuilds the KV
+ * cache of the stable prefix [0, k) by a local prefill; the source streams
+ * the per-layer K/V of completed suffix blocks with their logical positions;
+ * at handover the target copies them into a newly allocated block table
+ * (Section 5), checks that [0, n) is covered with no gap or conflict and
+ * that no block of a cancelled attempt (older migration epoch) enters the
+ * request, and resumes decoding at position n.
+ *
+ * Calls:
+ *   pallas_prefill_prefix      prefix prefill writing K/V into paged blocks
+ *   pallas_pack_suffix_blocks  gather suffix pages into transfer chunks
+ *   pallas_assemble_kv         scatter chunks into the target block table
+ *   pallas_decode_step         one decode step over an assembled cache
+ *   pallas_check_coverage      host-only [0, n) coverage check
+ *
+ * Conventions shared by every call:
+ *   - Device pointers are named d_*, host pointers h_*.  All device memory
+ *     (weights, pools, tables, chunk arenas, logits, workspace) belongs to the
+ *     caller; the library allocates no device memory and keeps no pointer
+ *     beyond a call, except the weight pointers kept by a model handle.
+ *   - Host structs and arrays are read during the call only.
+ *   - `stream` is a hipStream_t (NULL: the default stream).  Work is enqueued
+ *     on it; calls return before the work completes and never synchronise.
+ *   - A nonzero return is a pallas_status.  Every argument check is done
+ *     before anything is enqueued, so a rejected call writes nothing.
+ *     pallas_last_error() gives a message (thread-local, valid until the
+ *     thread's next call).
+ *   - Element type of weights, activations and the KV cache is bf16 (raw
+ *     16-bit patterns); the residual stream is float32; logits are float32.
+ *   - Results are bitwise reproducible run to run for the same inputs.
+ */
+#ifndef PALLAS_H
+#define PALLAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PALLAS_ABI_VERSION 1
+#define PALLAS_MAX_SEQS 64 /* sequences per prefill or decode call */
+
+typedef enum {
+  PALLAS_OK = 0,
+  PALLAS_ERR_INVALID_ARG = 1,  /* null pointer, bad size, shape mismatch */
+  PALLAS_ERR_OUT_OF_RANGE = 2, /* position or range outside a table / arena */
+  PALLAS_ERR_COVERAGE = 3,     /* gap or two claims on one position */
+  PALLAS_ERR_STALE_EPOCH = 4,  /* chunk of another migration epoch */
+  PALLAS_ERR_WRONG_REQUEST = 5,/* chunk of another request */
+  PALLAS_ERR_UNSUPPORTED = 6,  /* shape this build has no kernel for */
+  PALLAS_ERR_HIP = 7,          /* a HIP runtime call failed */
+  PALLAS_ERR_WORKSPACE = 8     /* workspace too small */
+} pallas_status;
+
+/* Device-side error bits written (OR-ed) into the optional d_err word. */
+#define PALLAS_DEVERR_PAGE 1u /* a block-table entry named no page of the pool;
+                                 that position was skipped */
+
+/* Decoder shape (Qwen3/Llama-style pre-norm decoder, Section 6.1 models). */
+typedef struct {
+  int32_t n_layers;
+  int32_t hidden;     /* H */
+  int32_t n_q_heads;  /* Hq */
+  int32_t n_kv_heads; /* Hkv; Hq must be a multiple of it */
+  int32_t head_dim;   /* d: 64 or 128 */
+  int32_t ffn;        /* F */
+  int32_t vocab;      /* V */
+  float rms_eps;      /* RMSNorm epsilon (all norms) */
+  float rope_theta;   /* rotary base */
+  int32_t qk_norm;    /* 1: per-head RMSNorm of Q and K before rotary */
+  int32_t page_size;  /* tokens per KV page; this build supports 16 */
+} pallas_model_config;
+
+/* Per-layer weights, device pointers to bf16, matrices row-major [out][in]:
+ *   attn_norm [H]; w_qkv [(Hq + 2 Hkv) d][H] (rows: Q heads, K heads,
+ *   V heads); q_norm [d]; k_norm [d] (ignored when qk_norm = 0);
+ *   w_o [H][Hq d]; mlp_norm [H]; w_gate_up [2F][H] (rows: gate, then up);
+ *   w_down [H][F].  Every pointer must be 16-byte aligned. */
+typedef struct {
+  const void* attn_norm;
+  const void* w_qkv;
+  const void* q_norm;
+  const void* k_norm;
+  const void* w_o;
+  const void* mlp_norm;
+  const void* w_gate_up;
+  const void* w_down;
+} pallas_layer_weights;
+
+/* Global weights: embed [V][H], final_norm [H], lm_head [V][H] (device,
+ * bf16); layers: host array of n_layers entries, copied at model creation. */
+typedef struct {
+  const void* embed;
+  const void* final_norm;
+  const void* lm_head;
+  const pallas_layer_weights* layers;
+} pallas_weights;
+
+/* A paged KV pool: bf16 [n_layers][2 (K, V)][num_pages][page_size]
+ * [n_kv_heads][head_dim] at `base` (device, 16-byte aligned).  K is stored
+ * after rotary embedding. */
+typedef struct {
+  void* base;
+  int32_t num_pages;
+  int32_t page_size;
+  int32_t n_layers;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+} pallas_kv_pool;
+
+/* One transfer chunk to pack: positions [start_pos, start_pos + num_tokens)
+ * of the source sequence, written as bf16 [L][2][num_tokens][Hkv][d] at byte
+ * offset arena_offset (16-byte aligned) of the chunk arena. */
+typedef struct {
+  int32_t start_pos;
+  int32_t num_tokens;
+  uint64_t arena_offset;
+} pallas_chunk_desc;
+
+/* A received chunk: what the source sent with it (Section 4.3: logical
+ * positions, request id, migration epoch) and where its payload
+ * bf16 [n_layers][2][num_tokens][n_kv_heads][head_dim] sits in the arena. */
+typedef struct {
+  uint64_t request_id;
+  uint64_t epoch;
+  int32_t start_pos;
+  int32_t num_tokens;
+  uint64_t arena_offset;
+  int32_t n_layers;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t elem_bytes;
+} pallas_chunk_header;
+
+typedef struct pallas_model pallas_model;
+
+/* ABI version of the loaded library (PALLAS_ABI_VERSION). */
+int32_t pallas_abi_version(void);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char* pallas_last_error(void);
+
+/* Create a model handle over caller-owned weights (pointers are kept, bytes
+ * are not copied).  Fails with INVALID_ARG on a null pointer or inconsistent
+ * shape and UNSUPPORTED on a shape without kernels (head_dim other than 64 or
+ * 128, page_size other than 16, hidden or ffn not a multiple of 64). */
+int pallas_model_create(const pallas_model_config* cfg, const pallas_weights* w,
+                        pallas_model** out);
+void pallas_model_destroy(pallas_model* m);
+
+/* Bytes of device workspace that prefill and decode need for up to
+ * `max_tokens` tokens over up to `max_seqs` sequences in one call. */
+size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t max_seqs);
+
+/* Prefix prefill (Section 4.3: the target rebuilds the KV cache of the
+ * stable prefix by local prefill; Section 5: an ordinary prefill).
+ *
+ * Sequence i holds the ids d_token_ids[h_cu_seqlens[i] .. h_cu_seqlens[i+1])
+ * (int32, device) at positions 0 .. p_i - 1.  For every layer, post-rotary K
+ * and V of each token t are written to
+ *   pool[l][0|1][bt_i[t / page]][t % page]
+ * with bt_i = d_block_tables + i * max_pages (int32, device).  Nothing else
+ * is written to the pool; no logits are produced.  num_seqs in
+ * [1, PALLAS_MAX_SEQS]; p_i >= 1; sum p_i <= the workspace's max_tokens.
+ * Table entries outside [0, num_pages) are skipped and raise
+ * PALLAS_DEVERR_PAGE in *d_err (nullable, device, caller clears it). */
+int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
+                          const int32_t* h_cu_seqlens, const int32_t* d_block_tables,
+                          int32_t max_pages, const pallas_kv_pool* pool, void* d_workspace,
+                          size_t ws_bytes, int32_t* d_err, void* stream);
+
+/* Suffix-block extraction (Section 4.3, Section 5: per-layer K/V of
+ * completed blocks, taken by physical block id from the GPU cache).
+ *
+ * For each descriptor j and position t in [start, start + num_tokens):
+ *   chunk_j[l][kv][t - start] = src[l][kv][bt[t / page]][t % page]
+ * with bt = d_src_block_table (int32 [max_pages], device).  One launch covers
+ * every descriptor.  Rejected (nothing written) when a range leaves
+ * [0, max_pages * page), a chunk leaves the arena or two chunks overlap in
+ * the arena.  Entries outside [0, num_pages) are skipped and raise
+ * PALLAS_DEVERR_PAGE in *d_err (nullable). */
+int pallas_pack_suffix_blocks(const pallas_kv_pool* src, const int32_t* d_src_block_table,
+                              int32_t max_pages, const pallas_chunk_desc* h_descs,
+                              int32_t n_descs, void* d_chunk_arena, size_t arena_bytes,
+                              int32_t* d_err, void* stream);
+
+/* Assembly into the target block table (Section 5: a new block table, then
+ * a copy of the buffered suffix blocks; Section 4.3: state consistency).
+ *
+ * Host checks, in this order, each rejecting the whole call before anything
+ * is enqueued: a header's shape differs from the pool (INVALID_ARG); its
+ * request id differs from expected_request_id (WRONG_REQUEST); its epoch
+ * differs from expected_epoch (STALE_EPOCH); its range leaves
+ * [0, max_pages * page) or its payload leaves the arena (OUT_OF_RANGE); two
+ * chunks claim one position (COVERAGE).  Then one launch writes
+ *   dst[l][kv][bt[t / page]][t % page] = chunk[l][kv][t - start]
+ * for every chunk and position; partial first and last pages are written
+ * slot by slot and other slots of those pages keep their contents.  Table
+ * entries outside [0, num_pages) are skipped and raise PALLAS_DEVERR_PAGE in
+ * *d_err (nullable). */
+int pallas_assemble_kv(const pallas_kv_pool* dst, const int32_t* d_dst_block_table,
+                       int32_t max_pages, const pallas_chunk_header* h_hdrs,
+                       const void* d_chunk_arena, size_t arena_bytes, int32_t n_chunks,
+                       uint64_t expected_request_id, uint64_t expected_epoch,
+                       int32_t* d_err, void* stream);
+
+/* One decode step per sequence over its assembled cache (Section 4.3: the
+ * target generates token n without repeating prefill over [0, n)).
+ *
+ * Sequence i feeds token d_tokens[i] (int32, device) at position
+ * h_positions[i] = n_i; it attends to cached positions [0, n_i) and to
+ * itself, writes its own K/V into slot n_i (the table needs capacity
+ * n_i + 1), and the float32 logits of the next token go to
+ * d_logits[i][0..V).  num_seqs in [1, PALLAS_MAX_SEQS]. */
+int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_tokens,
+                       const int32_t* h_positions, const int32_t* d_block_tables,
+                       int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,
+                       void* d_workspace, size_t ws_bytes, int32_t* d_err, void* stream);
+
+/* Coverage check (Section 4.3, "State consistency"), host only: returns
+ * PALLAS_OK iff [0, prefix_len) and the ranges [h_starts[j], h_starts[j] +
+ * h_lens[j]) together cover [0, n) exactly once (empty ranges are ignored),
+ * PALLAS_ERR_COVERAGE otherwise, PALLAS_ERR_INVALID_ARG on null arrays with
+ * n_ranges > 0 or negative lengths. */
+int pallas_check_coverage(int32_t prefix_len, const int32_t* h_starts, const int32_t* h_lens,
+                          int32_t n_ranges, int32_t n);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PALLAS_H */

@@ -1,0 +1,47 @@
+// Model handle and the per-call plan of the prefill and decode sequences.
+#pragma once
+
+#include <vector>
+
+#include "pallas.h"
+
+struct pallas_model {
+  pallas_model_config cfg;
+  const void* embed;
+  const void* final_norm;
+  const void* lm_head;
+  std::vector<pallas_layer_weights> layers;
+};
+
+namespace pallas {
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Workspace carve-up for `tokens` rows (prefill: sum of prefix lengths;
+// decode: number of sequences).
+struct Workspace {
+  size_t resid, h, qkv, q, o, act, rope, total;
+};
+
+inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens) {
+  Workspace w;
+  const int64_t qkv = int64_t(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  size_t at = 0;
+  auto take = [&](size_t bytes) { size_t o = at; at = align_up(at + bytes, 256); return o; };
+  w.resid = take(size_t(tokens) * c.hidden * 4);
+  w.h = take(size_t(tokens) * c.hidden * 2);
+  w.qkv = take(size_t(tokens) * qkv * 2);
+  w.q = take(size_t(tokens) * c.n_q_heads * c.head_dim * 2);
+  w.o = take(size_t(tokens) * c.n_q_heads * c.head_dim * 2);
+  w.act = take(size_t(tokens) * c.ffn * 2);
+  w.rope = take(size_t(tokens) * (c.head_dim / 2) * 8);  // (cos, sin) per row and pair
+  w.total = at;
+  return w;
+}
+
+inline size_t workspace_bytes(const pallas_model_config& c, int32_t max_tokens, int32_t max_seqs) {
+  (void)max_seqs;
+  return workspace_layout(c, max_tokens).total;
+}
+
+}  // namespace pallas

@@ -1,0 +1,298 @@
+// C ABI of the reconstruction library: argument checks, plans and launch
+// sequences.  Every check runs before anything is enqueued, so a rejected
+// call writes nothing.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "pallas.h"
+#include "kernels.h"
+#include "model_plan.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(PALLAS_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+int check_pool(const pallas_kv_pool* p, const char* what) {
+  if (!p) return fail(PALLAS_ERR_INVALID_ARG, "%s: null pool", what);
+  if (!p->base) return fail(PALLAS_ERR_INVALID_ARG, "%s: null pool base", what);
+  if (p->num_pages <= 0 || p->page_size <= 0 || p->n_layers <= 0 || p->n_kv_heads <= 0 ||
+      p->head_dim <= 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: non-positive pool dimension", what);
+  if ((reinterpret_cast<uintptr_t>(p->base) & 15) != 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: pool base not 16-byte aligned", what);
+  const int64_t row = int64_t(p->n_kv_heads) * p->head_dim * 2;
+  if (row % 16 != 0 || row > (1 << 30))
+    return fail(PALLAS_ERR_UNSUPPORTED, "%s: K/V row of %lld bytes is not a multiple of 16", what,
+                (long long)row);
+  return PALLAS_OK;
+}
+
+pallas::PoolGeom geom_of(const pallas_kv_pool* p) {
+  pallas::PoolGeom g;
+  g.base = static_cast<char*>(p->base);
+  g.num_pages = p->num_pages;
+  g.page = p->page_size;
+  g.lk = 2 * p->n_layers;
+  g.row_bytes = p->n_kv_heads * p->head_dim * 2;
+  return g;
+}
+
+struct Span {
+  int64_t a, b;
+  int idx;
+};
+
+// Splits the non-empty ranges into launches of at most kCopyMaxChunks chunks.
+int run_copies(bool pack, const pallas::PoolGeom& g, const int32_t* bt, char* arena,
+               const std::vector<pallas::CopyChunk>& chunks, int32_t* d_err, hipStream_t s) {
+  size_t i = 0;
+  while (i < chunks.size()) {
+    pallas::CopyBatch b;
+    b.n = 0;
+    b.unit_prefix[0] = 0;
+    int64_t units = 0;
+    for (; i < chunks.size() && b.n < pallas::kCopyMaxChunks; ++i) {
+      const pallas::CopyChunk& c = chunks[i];
+      const int64_t nb = (c.count + pallas::kCopyTokens - 1) / pallas::kCopyTokens;
+      const int64_t add = nb * g.lk;
+      if (b.n > 0 && units + add > (int64_t(1) << 30)) break;
+      b.c[b.n] = c;
+      units += add;
+      b.n += 1;
+      b.unit_prefix[b.n] = static_cast<int32_t>(units);
+    }
+    hipError_t e = pallas::launch_kv_copy(pack, g, bt, arena, b, d_err, s);
+    if (e != hipSuccess) return hip_fail(e, pack ? "pack launch" : "assemble launch");
+  }
+  return PALLAS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t pallas_abi_version(void) { return PALLAS_ABI_VERSION; }
+
+const char* pallas_last_error(void) { return g_err.c_str(); }
+
+int pallas_check_coverage(int32_t prefix_len, const int32_t* h_starts, const int32_t* h_lens,
+                          int32_t n_ranges, int32_t n) {
+  if (n_ranges < 0 || (n_ranges > 0 && (!h_starts || !h_lens)))
+    return fail(PALLAS_ERR_INVALID_ARG, "coverage: bad range arrays");
+  if (prefix_len < 0 || n < 0 || prefix_len > n)
+    return fail(PALLAS_ERR_COVERAGE, "coverage: prefix %d outside [0, %d]", prefix_len, n);
+  std::vector<Span> spans;
+  for (int j = 0; j < n_ranges; ++j) {
+    if (h_lens[j] < 0) return fail(PALLAS_ERR_INVALID_ARG, "coverage: negative length");
+    if (h_lens[j] == 0) continue;
+    spans.push_back({h_starts[j], int64_t(h_starts[j]) + h_lens[j], j});
+  }
+  std::sort(spans.begin(), spans.end(), [](const Span& x, const Span& y) { return x.a < y.a; });
+  int64_t at = prefix_len;
+  for (const Span& sp : spans) {
+    if (sp.a < at) return fail(PALLAS_ERR_COVERAGE, "coverage: position %lld claimed twice", (long long)sp.a);
+    if (sp.a > at) return fail(PALLAS_ERR_COVERAGE, "coverage: gap at %lld", (long long)at);
+    at = sp.b;
+  }
+  if (at != n) return fail(PALLAS_ERR_COVERAGE, "coverage: covered [0, %lld) of [0, %d)", (long long)at, n);
+  return PALLAS_OK;
+}
+
+int pallas_pack_suffix_blocks(const pallas_kv_pool* src, const int32_t* d_src_block_table,
+                              int32_t max_pages, const pallas_chunk_desc* h_descs,
+                              int32_t n_descs, void* d_chunk_arena, size_t arena_bytes,
+                              int32_t* d_err, void* stream) {
+  if (int rc = check_pool(src, "pack")) return rc;
+  if (!d_src_block_table || max_pages <= 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "pack: null block table or max_pages <= 0");
+  if (n_descs < 0 || (n_descs > 0 && !h_descs))
+    return fail(PALLAS_ERR_INVALID_ARG, "pack: bad descriptor array");
+  const pallas::PoolGeom g = geom_of(src);
+  const int64_t cap = int64_t(max_pages) * src->page_size;
+  const int64_t tok_bytes = int64_t(g.lk) * g.row_bytes;
+  std::vector<pallas::CopyChunk> chunks;
+  std::vector<Span> spans;
+  for (int j = 0; j < n_descs; ++j) {
+    const pallas_chunk_desc& d = h_descs[j];
+    if (d.start_pos < 0 || d.num_tokens < 0 || int64_t(d.start_pos) + d.num_tokens > cap)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "pack: chunk %d range [%d, +%d) outside the table (%lld)",
+                  j, d.start_pos, d.num_tokens, (long long)cap);
+    if (d.num_tokens == 0) continue;
+    if (d.arena_offset % 16 != 0)
+      return fail(PALLAS_ERR_INVALID_ARG, "pack: chunk %d arena offset not 16-byte aligned", j);
+    const uint64_t bytes = uint64_t(d.num_tokens) * tok_bytes;
+    if (!d_chunk_arena || d.arena_offset > arena_bytes || bytes > arena_bytes - d.arena_offset)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "pack: chunk %d leaves the arena", j);
+    spans.push_back({int64_t(d.arena_offset), int64_t(d.arena_offset + bytes), j});
+    chunks.push_back({d.start_pos, d.num_tokens, d.arena_offset});
+  }
+  std::sort(spans.begin(), spans.end(), [](const Span& x, const Span& y) { return x.a < y.a; });
+  for (size_t k = 1; k < spans.size(); ++k)
+    if (spans[k].a < spans[k - 1].b)
+      return fail(PALLAS_ERR_INVALID_ARG, "pack: chunks %d and %d overlap in the arena",
+                  spans[k - 1].idx, spans[k].idx);
+  return run_copies(true, g, d_src_block_table, static_cast<char*>(d_chunk_arena), chunks, d_err,
+                    static_cast<hipStream_t>(stream));
+}
+
+int pallas_assemble_kv(const pallas_kv_pool* dst, const int32_t* d_dst_block_table,
+                       int32_t max_pages, const pallas_chunk_header* h_hdrs,
+                       const void* d_chunk_arena, size_t arena_bytes, int32_t n_chunks,
+                       uint64_t expected_request_id, uint64_t expected_epoch, int32_t* d_err,
+                       void* stream) {
+  if (int rc = check_pool(dst, "assemble")) return rc;
+  if (!d_dst_block_table || max_pages <= 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "assemble: null block table or max_pages <= 0");
+  if (n_chunks < 0 || (n_chunks > 0 && !h_hdrs))
+    return fail(PALLAS_ERR_INVALID_ARG, "assemble: bad header array");
+  for (int j = 0; j < n_chunks; ++j) {
+    const pallas_chunk_header& h = h_hdrs[j];
+    if (h.n_layers != dst->n_layers || h.n_kv_heads != dst->n_kv_heads ||
+        h.head_dim != dst->head_dim || h.elem_bytes != 2)
+      return fail(PALLAS_ERR_INVALID_ARG, "assemble: chunk %d shape differs from the pool", j);
+  }
+  for (int j = 0; j < n_chunks; ++j)
+    if (h_hdrs[j].request_id != expected_request_id)
+      return fail(PALLAS_ERR_WRONG_REQUEST, "assemble: chunk %d belongs to request %llu, not %llu", j,
+                  (unsigned long long)h_hdrs[j].request_id, (unsigned long long)expected_request_id);
+  for (int j = 0; j < n_chunks; ++j)
+    if (h_hdrs[j].epoch != expected_epoch)
+      return fail(PALLAS_ERR_STALE_EPOCH, "assemble: chunk %d has epoch %llu, expected %llu", j,
+                  (unsigned long long)h_hdrs[j].epoch, (unsigned long long)expected_epoch);
+  const pallas::PoolGeom g = geom_of(dst);
+  const int64_t cap = int64_t(max_pages) * dst->page_size;
+  const int64_t tok_bytes = int64_t(g.lk) * g.row_bytes;
+  std::vector<pallas::CopyChunk> chunks;
+  std::vector<Span> spans;
+  for (int j = 0; j < n_chunks; ++j) {
+    const pallas_chunk_header& h = h_hdrs[j];
+    if (h.start_pos < 0 || h.num_tokens < 0 || int64_t(h.start_pos) + h.num_tokens > cap)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "assemble: chunk %d range [%d, +%d) outside the table (%lld)",
+                  j, h.start_pos, h.num_tokens, (long long)cap);
+    if (h.num_tokens == 0) continue;
+    const uint64_t bytes = uint64_t(h.num_tokens) * tok_bytes;
+    if (!d_chunk_arena || h.arena_offset > arena_bytes || bytes > arena_bytes - h.arena_offset)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "assemble: chunk %d payload leaves the arena", j);
+    if (h.arena_offset % 16 != 0)
+      return fail(PALLAS_ERR_INVALID_ARG, "assemble: chunk %d arena offset not 16-byte aligned", j);
+    spans.push_back({h.start_pos, int64_t(h.start_pos) + h.num_tokens, j});
+    chunks.push_back({h.start_pos, h.num_tokens, h.arena_offset});
+  }
+  std::sort(spans.begin(), spans.end(), [](const Span& x, const Span& y) { return x.a < y.a; });
+  for (size_t k = 1; k < spans.size(); ++k)
+    if (spans[k].a < spans[k - 1].b)
+      return fail(PALLAS_ERR_COVERAGE, "assemble: chunks %d and %d both claim position %lld",
+                  spans[k - 1].idx, spans[k].idx, (long long)spans[k].a);
+  return run_copies(false, g, d_dst_block_table,
+                    const_cast<char*>(static_cast<const char*>(d_chunk_arena)), chunks, d_err,
+                    static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ model
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int check_cfg(const pallas_model_config* c) {
+  if (c->n_layers <= 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->ffn <= 0 || c->vocab <= 0 || c->page_size <= 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "model: non-positive dimension");
+  if (c->n_q_heads % c->n_kv_heads != 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "model: query heads not a multiple of KV heads");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f))
+    return fail(PALLAS_ERR_INVALID_ARG, "model: bad eps or rope theta");
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(PALLAS_ERR_UNSUPPORTED, "model: head_dim %d (supported: 64, 128)", c->head_dim);
+  if (c->page_size != 16)
+    return fail(PALLAS_ERR_UNSUPPORTED, "model: page_size %d (supported: 16)", c->page_size);
+  if (c->hidden % 64 != 0 || c->ffn % 16 != 0)
+    return fail(PALLAS_ERR_UNSUPPORTED, "model: hidden must be a multiple of 64 and ffn of 16");
+  if (c->n_q_heads / c->n_kv_heads > 16)
+    return fail(PALLAS_ERR_UNSUPPORTED, "model: more than 16 query heads per KV head");
+  return PALLAS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int pallas_model_create(const pallas_model_config* cfg, const pallas_weights* w,
+                        pallas_model** out) {
+  if (!cfg || !w || !out) return fail(PALLAS_ERR_INVALID_ARG, "model: null argument");
+  *out = nullptr;
+  if (int rc = check_cfg(cfg)) return rc;
+  if (!w->embed || !w->final_norm || !w->lm_head || !w->layers)
+    return fail(PALLAS_ERR_INVALID_ARG, "model: null global weight");
+  if (!aligned16(w->embed) || !aligned16(w->lm_head))
+    return fail(PALLAS_ERR_INVALID_ARG, "model: weights must be 16-byte aligned");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const pallas_layer_weights& L = w->layers[l];
+    const void* need[] = {L.attn_norm, L.w_qkv, L.w_o, L.mlp_norm, L.w_gate_up, L.w_down};
+    for (const void* p : need)
+      if (!p || !aligned16(p)) return fail(PALLAS_ERR_INVALID_ARG, "model: layer %d weight null or unaligned", l);
+    if (cfg->qk_norm && (!L.q_norm || !L.k_norm))
+      return fail(PALLAS_ERR_INVALID_ARG, "model: layer %d lacks QK-norm gains", l);
+  }
+  pallas_model* m = new pallas_model;
+  m->cfg = *cfg;
+  m->embed = w->embed;
+  m->final_norm = w->final_norm;
+  m->lm_head = w->lm_head;
+  m->layers.assign(w->layers, w->layers + cfg->n_layers);
+  *out = m;
+  return PALLAS_OK;
+}
+
+void pallas_model_destroy(pallas_model* m) { delete m; }
+
+}  // extern "C"
+
+// ------------------------------------------------------------- prefill / decode
+extern "C" {
+
+size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t max_seqs) {
+  if (!m || max_tokens <= 0 || max_seqs <= 0) return 0;
+  return pallas::workspace_bytes(m->cfg, max_tokens, max_seqs);
+}
+
+int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
+                          const int32_t* h_cu_seqlens, const int32_t* d_block_tables,
+                          int32_t max_pages, const pallas_kv_pool* pool, void* d_workspace,
+                          size_t ws_bytes, int32_t* d_err, void* stream) {
+  (void)m; (void)num_seqs; (void)d_token_ids; (void)h_cu_seqlens; (void)d_block_tables;
+  (void)max_pages; (void)pool; (void)d_workspace; (void)ws_bytes; (void)d_err; (void)stream;
+  return fail(PALLAS_ERR_UNSUPPORTED, "prefill: not built yet");
+}
+
+int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_tokens,
+                       const int32_t* h_positions, const int32_t* d_block_tables,
+                       int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,
+                       void* d_workspace, size_t ws_bytes, int32_t* d_err, void* stream) {
+  (void)m; (void)num_seqs; (void)d_tokens; (void)h_positions; (void)d_block_tables;
+  (void)max_pages; (void)pool; (void)d_logits; (void)d_workspace; (void)ws_bytes; (void)d_err;
+  (void)stream;
+  return fail(PALLAS_ERR_UNSUPPORTED, "decode: not built yet");
+}
+
+}  // extern "C"

@@ -1,0 +1,132 @@
+"""The C-ABI library loads, exports every call the header declares, and its
+host-side logic (coverage check, argument and consistency checks that run
+before anything is enqueued) agrees with the oracle.  No GPU needed: every
+call here is rejected before it touches device memory."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from helpers import ensure_lib
+from oracle import paged
+import test_oracle_paged as top
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000  # a non-null, aligned address that no call here dereferences
+
+
+@pytest.fixture(scope="module")
+def P():
+    return ensure_lib()
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "pallas.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(pallas_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_call(P):
+    names = header_functions()
+    assert "pallas_prefill_prefix" in names and "pallas_assemble_kv" in names
+    h = P.lib()
+    for n in names:
+        assert hasattr(h, n), n
+    assert set(names) == set(P.EXPORTS), "binding and header disagree"
+    assert P.pallas_abi_version() == 1
+
+
+@pytest.mark.parametrize("prefix,ranges,n,ok", top.test_check_coverage.pytestmark[0].args[1])
+def test_coverage_matches_oracle(P, prefix, ranges, n, ok):
+    st = P.pallas_check_coverage(prefix, [r[0] for r in ranges], [r[1] for r in ranges], n)
+    want = paged.check_coverage(prefix, [r[0] for r in ranges], [r[1] for r in ranges], n)
+    assert want is ok
+    assert (st == P.Status.OK) is ok
+    if not ok:
+        assert st == P.Status.COVERAGE
+        assert "coverage" in P.pallas_last_error()
+
+
+def fake_pool(P, L=2, pages=8, page=16, hkv=2, d=64):
+    from paper_2608_16477_amd.binding import KVPoolC
+    return KVPoolC(FAKE, pages, page, L, hkv, d)
+
+
+def assemble_rc(P, hdrs, req=7, epoch=3, max_pages=4, arena_bytes=1 << 30):
+    h = P.lib()
+    arr = (P.ChunkHeader * len(hdrs))(*hdrs)
+    pool = fake_pool(P)
+    return h.pallas_assemble_kv(C.byref(pool), FAKE, max_pages, arr, FAKE, arena_bytes,
+                                len(hdrs), req, epoch, None, None)
+
+
+def hdr(P, start, cnt, req=7, epoch=3, off=0, shape=(2, 2, 64)):
+    return P.ChunkHeader(req, epoch, start, cnt, off, *shape, 2)
+
+
+@pytest.mark.parametrize("case,code", [
+    ("request", "WRONG_REQUEST"), ("epoch", "STALE_EPOCH"), ("shape", "INVALID_ARG"),
+    ("range", "OUT_OF_RANGE"), ("overlap", "COVERAGE"), ("arena", "OUT_OF_RANGE"),
+])
+def test_assemble_host_rejections_match_oracle(P, case, code):
+    row = 2 * 2 * 64 * 2   # bytes per position over 2 layers x K|V
+    good = hdr(P, 0, 16)
+    bad = {
+        "request": hdr(P, 16, 8, req=8, off=16 * row),
+        "epoch": hdr(P, 16, 8, epoch=2, off=16 * row),
+        "shape": hdr(P, 16, 8, off=16 * row, shape=(2, 2, 128)),
+        "range": hdr(P, 60, 8, off=16 * row),
+        "overlap": hdr(P, 15, 8, off=16 * row),
+        "arena": hdr(P, 16, 8, off=(1 << 30) - row),
+    }[case]
+    rc = assemble_rc(P, [good, bad])
+    assert P.Status(rc).name == code, P.pallas_last_error()
+    if case != "arena":   # the oracle has no arena; the other rules are shared
+        oh = [paged.ChunkHeader(x.request_id, x.epoch, x.start_pos, x.num_tokens, x.n_layers,
+                                x.n_kv_heads, x.head_dim, x.elem_bytes) for x in (good, bad)]
+        import numpy as np
+        pool = np.zeros((2, 2, 8, 16, 2, 64), np.uint16)
+        with pytest.raises(paged.Rejected) as e:
+            paged.check_chunks(pool, 4 * 16, oh, 7, 3)
+        assert e.value.code == code
+
+
+def test_pack_host_rejections(P):
+    h = P.lib()
+    pool = fake_pool(P)
+    def rc(descs, arena_bytes=1 << 20, max_pages=4):
+        arr = (P.ChunkDesc * max(1, len(descs)))(*descs)
+        return P.Status(h.pallas_pack_suffix_blocks(C.byref(pool), FAKE, max_pages, arr, len(descs),
+                                                    FAKE, arena_bytes, None, None))
+    row = 2 * 2 * 64 * 2
+    assert rc([P.ChunkDesc(60, 8, 0)]) == P.Status.OUT_OF_RANGE
+    assert rc([P.ChunkDesc(0, 8, 8)]) == P.Status.INVALID_ARG             # unaligned offset
+    assert rc([P.ChunkDesc(0, 8, 0)], arena_bytes=8 * row - 16) == P.Status.OUT_OF_RANGE
+    assert rc([P.ChunkDesc(0, 8, 0), P.ChunkDesc(8, 8, 4 * row)]) == P.Status.INVALID_ARG  # arena overlap
+    assert rc([P.ChunkDesc(-1, 8, 0)]) == P.Status.OUT_OF_RANGE
+
+
+def test_model_create_rejects_bad_shapes(P):
+    from workloads import configs
+    from paper_2608_16477_amd.binding import ModelConfigC, WeightsC, LayerWeightsC
+    h = P.lib()
+    def rc(**kw):
+        c = configs.TINY.replace(**kw)
+        cc = ModelConfigC(c.n_layers, c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn,
+                          c.vocab, c.rms_eps, c.rope_theta, int(c.qk_norm), c.page_size)
+        la = (LayerWeightsC * c.n_layers)()
+        for l in range(c.n_layers):
+            for name, _ in LayerWeightsC._fields_:
+                setattr(la[l], name, FAKE)
+        w = WeightsC(FAKE, FAKE, FAKE, la)
+        out = C.c_void_p()
+        r = h.pallas_model_create(C.byref(cc), C.byref(w), C.byref(out))
+        if r == 0:
+            h.pallas_model_destroy(out)
+        return P.Status(r)
+    assert rc() == P.Status.OK
+    assert rc(n_q_heads=3) == P.Status.INVALID_ARG
+    assert rc(head_dim=96) == P.Status.UNSUPPORTED
+    assert rc(page_size=32) == P.Status.UNSUPPORTED
+    assert rc(hidden=200) == P.Status.UNSUPPORTED
