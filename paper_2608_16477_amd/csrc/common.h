@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "pallas.h"
+
 namespace pallas {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));

@@ -1,0 +1,215 @@
+// bf16 GEMM on gfx950 matrix cores: C = A * B^T with both operands K-major
+// (activations [M][K], weights [N][K] as stored, [out][in]) and a float32
+// accumulator, with the epilogue fused into the store.
+//
+// Tiling: a 256 x 256 output tile per workgroup of 4 waves, each wave
+// 128 x 128 as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at
+// a time through a double-buffered LDS stage (2 x (32 KiB A + 32 KiB B))
+// filled by buffer loads that write LDS directly (no register staging); the
+// buffer range check turns rows past M/N and columns past K into zeros.
+// LDS rows are 8 chunks of 16 bytes with the chunk index XOR-swizzled by
+// (row / 2) mod 8, so the 16-byte fragment reads of 16 consecutive rows hit
+// 16 distinct 4-bank groups.
+//
+// Workgroups are dispatched round-robin over the 8 XCDs; the tile index is
+// remapped so each XCD owns a contiguous run of tiles, M-tile fastest, so
+// the workgroups sharing one weight panel run on one XCD and share its L2.
+#include "common.h"
+#include "kernels.h"
+
+namespace pallas {
+
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int kThreads = 256;
+constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
+constexpr int kSlots = BM * kChunks;     // 16-byte slots per operand tile
+constexpr int kXcds = 8;
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 7)); }
+
+__device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
+                                              const int* row_off_valid, const int* chunk, int k0,
+                                              int K, u32x4* lds_tile, int wave, int lane) {
+  // 8 instructions per wave; instruction i fills slots [(wave*8+i)*64, +64).
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int base = (wave * 8 + i) * 64;
+    const int k = k0 + chunk[i] * 8;
+    const uint32_t off = (row_off_valid[i] >= 0 && k < K)
+                             ? static_cast<uint32_t>(row_off_valid[i]) + static_cast<uint32_t>(k) * 2u
+                             : limit;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_tile + base), 16, off, 0, 0, 0);
+  }
+  (void)lane;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) u32x4 lds[2][2][kSlots];  // [buf][A|B][slot]
+
+  const int bid = blockIdx.x;
+  const int loc = bid / kXcds;
+  if (loc >= p.tiles_per_xcd) return;
+  const int t = (bid % kXcds) * p.tiles_per_xcd + loc;
+  if (t >= p.total_tiles) return;
+  const int tm = t % p.tiles_m, tn = t / p.tiles_m;
+  const int m0 = tm * BM;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int g = lane >> 5, l32 = lane & 31;
+
+  // Per-thread load plan: row byte offsets (or -1 when out of range) and
+  // source chunk of the LDS slot each load instruction fills.
+  int a_off[8], b_off[8], chunk[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int s = (wave * 8 + i) * 64 + lane;
+    const int row = s / kChunks;
+    chunk[i] = (s % kChunks) ^ ((row >> 1) & 7);
+    const int gm = m0 + row;
+    a_off[i] = gm < p.M ? gm * p.lda * 2 : -1;
+    int gn;
+    bool ok;
+    if (EPI == kEpiSwiGLU) {
+      // tile rows [0,128): gate rows o0 + r; [128,256): up rows F + o0 + r - 128
+      const int o = tn * (BN / 2) + (row & 127);
+      ok = o < p.N;
+      gn = (row < 128) ? o : p.N + o;
+    } else {
+      gn = tn * BN + row;
+      ok = gn < p.N;
+    }
+    b_off[i] = ok ? gn * p.ldb * 2 : -1;
+  }
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)p.A, 0, p.a_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)p.B, 0, p.b_bytes, 0x00020000);
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+
+  const int wm = wave >> 1, wn = wave & 1;
+  // LDS row of this lane's A fragment i and B fragment j
+  int arow[4], brow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) arow[i] = wm * 128 + i * 32 + l32;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    brow[j] = (EPI == kEpiSwiGLU ? (j >> 1) * 128 + wn * 64 + (j & 1) * 32 : wn * 128 + j * 32) + l32;
+
+  const int KT = (p.K + BK - 1) / BK;
+  load_tile_lds(ra, p.a_bytes, a_off, chunk, 0, p.K, lds[0][0], wave, lane);
+  load_tile_lds(rb, p.b_bytes, b_off, chunk, 0, p.K, lds[0][1], wave, lane);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) {
+      load_tile_lds(ra, p.a_bytes, a_off, chunk, (kt + 1) * BK, p.K, lds[buf ^ 1][0], wave, lane);
+      load_tile_lds(rb, p.b_bytes, b_off, chunk, (kt + 1) * BK, p.K, lds[buf ^ 1][1], wave, lane);
+    }
+    const u32x4* At = lds[buf][0];
+    const u32x4* Bt = lds[buf][1];
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int c = kk * 2 + g;
+      bf16x8 a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = __builtin_bit_cast(bf16x8, At[swz(arow[i], c)]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+
+  // Epilogue.  Accumulator register r of block (i, j) holds
+  // row wm*128 + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+      if (row >= p.M) continue;
+      if (EPI == kEpiSwiGLU) {
+        uint16_t* C = static_cast<uint16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc;
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int col = tn * (BN / 2) + wn * 64 + jj * 32 + l32;
+          if (col < p.N) {
+            const float gt = acc[i][jj][r], up = acc[i][jj + 2][r];
+            C[col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int col = tn * BN + wn * 128 + j * 32 + l32;
+          if (col >= p.N) continue;
+          if (EPI == kEpiAddF32) {
+            float* C = static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc;
+            C[col] += acc[i][j][r];
+          } else if (EPI == kEpiF32) {
+            float* C = static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc;
+            C[col] = acc[i][j][r];
+          } else {
+            uint16_t* C = static_cast<uint16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc;
+            C[col] = f2bf(acc[i][j][r]);
+          }
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
+                       int ldc, int M, int N, int K, hipStream_t s) {
+  const int64_t brows64 = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
+  // byte offsets are 32-bit (buffer addressing): both operands below 2 GiB
+  if (int64_t(M) * lda * 2 >= (int64_t(1) << 31) || brows64 * ldb * 2 >= (int64_t(1) << 31) ||
+      M <= 0 || N <= 0 || K <= 0 || K % 8 != 0)
+    return hipErrorInvalidValue;
+  GemmParams p;
+  p.A = A;
+  p.B = B;
+  p.C = C;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.lda = lda;
+  p.ldb = ldb;
+  p.ldc = ldc;
+  p.tiles_m = (M + BM - 1) / BM;
+  p.tiles_n = epi == kEpiSwiGLU ? (N + BN / 2 - 1) / (BN / 2) : (N + BN - 1) / BN;
+  p.total_tiles = p.tiles_m * p.tiles_n;
+  p.tiles_per_xcd = (p.total_tiles + kXcds - 1) / kXcds;
+  p.a_bytes = static_cast<uint32_t>(int64_t(M) * lda * 2);
+  const int64_t brows = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
+  p.b_bytes = static_cast<uint32_t>(brows * ldb * 2);
+  const int grid = p.tiles_per_xcd * kXcds;
+  switch (epi) {
+    case kEpiBf16: gemm_bf16_kernel<kEpiBf16><<<grid, kThreads, 0, s>>>(p); break;
+    case kEpiAddF32: gemm_bf16_kernel<kEpiAddF32><<<grid, kThreads, 0, s>>>(p); break;
+    case kEpiSwiGLU: gemm_bf16_kernel<kEpiSwiGLU><<<grid, kThreads, 0, s>>>(p); break;
+    case kEpiF32: gemm_bf16_kernel<kEpiF32><<<grid, kThreads, 0, s>>>(p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace pallas

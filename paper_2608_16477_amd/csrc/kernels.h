@@ -36,3 +36,109 @@ hipError_t launch_kv_copy(bool pack, const PoolGeom& pool, const int32_t* bt, ch
                           const CopyBatch& b, int32_t* d_err, hipStream_t s);
 
 }  // namespace pallas
+
+namespace pallas {
+
+// ---------------------------------------------------------------- GEMM
+enum GemmEpi : int {
+  kEpiBf16 = 0,    // C bf16 [M][ldc] = A B^T
+  kEpiAddF32 = 1,  // C f32 [M][ldc] += A B^T (residual add)
+  kEpiSwiGLU = 2,  // C bf16 [M][ldc] = silu(A Bg^T) * (A Bu^T); B rows [0,N) gate, [N,2N) up
+  kEpiF32 = 3,     // C f32 [M][ldc] = A B^T
+};
+
+struct GemmParams {
+  const uint16_t* A;
+  const uint16_t* B;
+  void* C;
+  int M, N, K;
+  int lda, ldb, ldc;
+  int tiles_m, tiles_n, total_tiles, tiles_per_xcd;
+  uint32_t a_bytes, b_bytes;
+};
+
+// A bf16 [M][lda] (K columns used), B bf16 [rows][ldb]; K a multiple of 8;
+// A and B 16-byte aligned; M*lda*2 and rows*ldb*2 below 4 GiB.
+hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
+                       int ldc, int M, int N, int K, hipStream_t s);
+
+}  // namespace pallas
+
+namespace pallas {
+
+// ------------------------------------------------------------ row metadata
+constexpr int kMaxSeqs = 64;
+
+// Rows [cu[s], cu[s+1]) belong to sequence s and sit at positions
+// base_pos[s] + (row - cu[s]); sequence s uses block-table row s.
+struct RowMap {
+  int32_t n_seqs;
+  int32_t cu[kMaxSeqs + 1];
+  int32_t base_pos[kMaxSeqs];
+};
+
+__host__ __device__ inline int row_seq(const RowMap& rm, int row) {
+  int s = 0;
+  while (s + 1 < rm.n_seqs && rm.cu[s + 1] <= row) ++s;
+  return s;
+}
+
+// ------------------------------------------------------------ norms / embed
+// r[t] = float(E[ids[t]]); h[t] = bf16(rmsnorm(r[t]) * g)
+hipError_t launch_embed_rmsnorm(const int32_t* ids, const uint16_t* embed, const uint16_t* gain,
+                                float* r, uint16_t* h, int rows, int H, float eps, int vocab,
+                                int32_t* err, hipStream_t s);
+// h[t] = bf16(rmsnorm(r[t]) * g)
+hipError_t launch_rmsnorm(const float* r, const uint16_t* gain, uint16_t* h, int rows, int H,
+                          float eps, hipStream_t s);
+
+// ------------------------------------------------------------ rotary table
+// tab[t][i] = (cos, sin)(pos(t) * theta^(-2i/d)), evaluated in double
+hipError_t launch_rope_table(const RowMap& rm, int rows, int d, float theta, float* tab,
+                             hipStream_t s);
+
+// ------------------------------------------------------------ QKV epilogue
+struct QkvParams {
+  const uint16_t* qkv;     // [rows][qkv_ld]: Q heads, K heads, V heads (or K, V only)
+  int qkv_ld;
+  int kv_only;             // 1: qkv holds only the K and V heads
+  const uint16_t* q_gain;  // [d] or null
+  const uint16_t* k_gain;  // [d] or null
+  const float* rope;       // [rows][d/2][2]
+  uint16_t* q_out;         // [rows][Hq][d] (unused when kv_only)
+  uint16_t* k_plane;       // pool K plane of this layer: [P][page][Hkv][d]
+  uint16_t* v_plane;       // pool V plane
+  const int32_t* bt;       // [n_seqs][max_pages]
+  int max_pages, num_pages, page;
+  int Hq, Hkv, d;
+  float eps;
+  int qk_norm;
+  int32_t* err;
+};
+hipError_t launch_qkv_rope(const QkvParams& p, const RowMap& rm, int rows, hipStream_t s);
+
+// ------------------------------------------------------------ attention
+struct AttnParams {
+  const uint16_t* q;       // [rows][Hq][d]
+  const uint16_t* k_plane; // [P][page][Hkv][d]
+  const uint16_t* v_plane;
+  const int32_t* bt;
+  int max_pages, num_pages, page;
+  uint16_t* o;             // [rows][Hq * d]
+  int Hq, Hkv, d;
+  float scale_log2;        // log2(e) / sqrt(d)
+};
+// Causal prefill attention: every row attends to keys of its own sequence at
+// positions <= its own (positions start at base_pos = 0).
+hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipStream_t s);
+// Decode attention: one row per sequence at position base_pos[s], keys
+// [0, base_pos[s]] through the table.
+// Needs base_pos[s] < 32768.
+hipError_t launch_attention_decode(const AttnParams& p, const RowMap& rm, hipStream_t s);
+
+// ------------------------------------------------------------ skinny GEMM
+// C[m][n] (op) A[m] . B[n] for m < M <= 8 rows; epilogues as launch_gemm.
+hipError_t launch_gemv(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
+                       int ldc, int M, int N, int K, hipStream_t s);
+
+}  // namespace pallas

@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <cmath>
 #include <vector>
 
 #include "pallas.h"
@@ -228,8 +229,8 @@ int check_cfg(const pallas_model_config* c) {
     return fail(PALLAS_ERR_UNSUPPORTED, "model: page_size %d (supported: 16)", c->page_size);
   if (c->hidden % 64 != 0 || c->ffn % 16 != 0)
     return fail(PALLAS_ERR_UNSUPPORTED, "model: hidden must be a multiple of 64 and ffn of 16");
-  if (c->n_q_heads / c->n_kv_heads > 16)
-    return fail(PALLAS_ERR_UNSUPPORTED, "model: more than 16 query heads per KV head");
+  if (c->n_q_heads / c->n_kv_heads > 8)
+    return fail(PALLAS_ERR_UNSUPPORTED, "model: more than 8 query heads per KV head");
   return PALLAS_OK;
 }
 
@@ -269,6 +270,206 @@ void pallas_model_destroy(pallas_model* m) { delete m; }
 }  // extern "C"
 
 // ------------------------------------------------------------- prefill / decode
+namespace {
+
+constexpr int kDecodeMaxPos = 16384;
+
+int check_model_pool(const pallas_model* m, const pallas_kv_pool* pool, const char* what) {
+  if (int rc = check_pool(pool, what)) return rc;
+  const pallas_model_config& c = m->cfg;
+  if (pool->n_layers != c.n_layers || pool->n_kv_heads != c.n_kv_heads ||
+      pool->head_dim != c.head_dim || pool->page_size != c.page_size)
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: pool shape differs from the model", what);
+  return PALLAS_OK;
+}
+
+int check_workspace(const pallas_model* m, const void* ws, size_t bytes, int64_t rows, const char* what) {
+  if (!ws) return fail(PALLAS_ERR_INVALID_ARG, "%s: null workspace", what);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", what);
+  const size_t need = pallas::workspace_layout(m->cfg, rows).total;
+  if (bytes < need)
+    return fail(PALLAS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", what, bytes, need);
+  return PALLAS_OK;
+}
+
+#define PALLAS_TRY(expr, where)                       \
+  do {                                                \
+    hipError_t e_ = (expr);                           \
+    if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+struct Planes {
+  uint16_t* k;
+  uint16_t* v;
+};
+
+Planes layer_planes(const pallas_kv_pool* pool, int l) {
+  const int64_t plane = int64_t(pool->num_pages) * pool->page_size * pool->n_kv_heads * pool->head_dim;
+  uint16_t* base = static_cast<uint16_t*>(pool->base) + int64_t(l) * 2 * plane;
+  return {base, base + plane};
+}
+
+const uint16_t* u16(const void* p) { return static_cast<const uint16_t*>(p); }
+
+// Projection of `rows` activation rows: the MFMA GEMM, or the skinny kernel
+// for up to 8 rows.
+hipError_t project(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C, int ldc,
+                   int rows, int N, int K, hipStream_t s) {
+  if (rows <= 8) return pallas::launch_gemv(epi, A, lda, B, ldb, C, ldc, rows, N, K, s);
+  return pallas::launch_gemm(epi, A, lda, B, ldb, C, ldc, rows, N, K, s);
+}
+
+int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const int32_t* ids,
+                const int32_t* bt, int max_pages, const pallas_kv_pool* pool, char* ws, int32_t* err,
+                hipStream_t s) {
+  const pallas_model_config& c = m->cfg;
+  const pallas::Workspace w = pallas::workspace_layout(c, M);
+  float* r = reinterpret_cast<float*>(ws + w.resid);
+  uint16_t* h = reinterpret_cast<uint16_t*>(ws + w.h);
+  uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + w.qkv);
+  uint16_t* q = reinterpret_cast<uint16_t*>(ws + w.q);
+  uint16_t* o = reinterpret_cast<uint16_t*>(ws + w.o);
+  uint16_t* act = reinterpret_cast<uint16_t*>(ws + w.act);
+  float* rope = reinterpret_cast<float*>(ws + w.rope);
+  const int H = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
+  const int QKV = (Hq + 2 * Hkv) * d, QD = Hq * d, KVD = 2 * Hkv * d;
+
+  PALLAS_TRY(pallas::launch_rope_table(rm, M, d, c.rope_theta, rope, s), "rope table");
+  PALLAS_TRY(pallas::launch_embed_rmsnorm(ids, u16(m->embed), u16(m->layers[0].attn_norm), r, h, M, H,
+                                          c.rms_eps, c.vocab, err, s), "embed");
+  pallas::QkvParams qp;
+  qp.rope = rope;
+  qp.q_out = q;
+  qp.bt = bt;
+  qp.max_pages = max_pages;
+  qp.num_pages = pool->num_pages;
+  qp.page = pool->page_size;
+  qp.Hq = Hq;
+  qp.Hkv = Hkv;
+  qp.d = d;
+  qp.eps = c.rms_eps;
+  qp.qk_norm = c.qk_norm;
+  qp.err = err;
+  pallas::AttnParams ap;
+  ap.q = q;
+  ap.bt = bt;
+  ap.max_pages = max_pages;
+  ap.num_pages = pool->num_pages;
+  ap.page = pool->page_size;
+  ap.o = o;
+  ap.Hq = Hq;
+  ap.Hkv = Hkv;
+  ap.d = d;
+  ap.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(d)));
+
+  for (int l = 0; l < c.n_layers; ++l) {
+    const pallas_layer_weights& L = m->layers[l];
+    const bool last = l == c.n_layers - 1;
+    const Planes pl = layer_planes(pool, l);
+    if (l > 0) PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.attn_norm), h, M, H, c.rms_eps, s), "rmsnorm");
+    qp.q_gain = u16(L.q_norm);
+    qp.k_gain = u16(L.k_norm);
+    qp.k_plane = pl.k;
+    qp.v_plane = pl.v;
+    if (last) {
+      // Only K and V of the last layer reach the cache.
+      PALLAS_TRY(pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv) + int64_t(QD) * H, H, qkv, KVD, M,
+                                     KVD, H, s), "kv gemm");
+      qp.qkv = qkv;
+      qp.qkv_ld = KVD;
+      qp.kv_only = 1;
+      PALLAS_TRY(pallas::launch_qkv_rope(qp, rm, M, s), "kv epilogue");
+      break;
+    }
+    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, M, QKV, H, s), "qkv gemm");
+    qp.qkv = qkv;
+    qp.qkv_ld = QKV;
+    qp.kv_only = 0;
+    PALLAS_TRY(pallas::launch_qkv_rope(qp, rm, M, s), "qkv epilogue");
+    ap.k_plane = pl.k;
+    ap.v_plane = pl.v;
+    PALLAS_TRY(pallas::launch_attention_prefill(ap, rm, s), "attention");
+    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, s), "o gemm");
+    PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, M, H, c.rms_eps, s), "rmsnorm");
+    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, M, F, H, s),
+               "gate_up gemm");
+    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, M, H, F, s), "down gemm");
+  }
+  return PALLAS_OK;
+}
+
+int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* tokens, const int32_t* bt,
+               int max_pages, const pallas_kv_pool* pool, float* logits, char* ws, int32_t* err,
+               hipStream_t s) {
+  const pallas_model_config& c = m->cfg;
+  const int B = rm.n_seqs;
+  const pallas::Workspace w = pallas::workspace_layout(c, B);
+  float* r = reinterpret_cast<float*>(ws + w.resid);
+  uint16_t* h = reinterpret_cast<uint16_t*>(ws + w.h);
+  uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + w.qkv);
+  uint16_t* q = reinterpret_cast<uint16_t*>(ws + w.q);
+  uint16_t* o = reinterpret_cast<uint16_t*>(ws + w.o);
+  uint16_t* act = reinterpret_cast<uint16_t*>(ws + w.act);
+  float* rope = reinterpret_cast<float*>(ws + w.rope);
+  const int H = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
+  const int QKV = (Hq + 2 * Hkv) * d, QD = Hq * d;
+
+  PALLAS_TRY(pallas::launch_rope_table(rm, B, d, c.rope_theta, rope, s), "rope table");
+  PALLAS_TRY(pallas::launch_embed_rmsnorm(tokens, u16(m->embed), u16(m->layers[0].attn_norm), r, h, B, H,
+                                          c.rms_eps, c.vocab, err, s), "embed");
+  pallas::QkvParams qp;
+  qp.rope = rope;
+  qp.q_out = q;
+  qp.bt = bt;
+  qp.max_pages = max_pages;
+  qp.num_pages = pool->num_pages;
+  qp.page = pool->page_size;
+  qp.Hq = Hq;
+  qp.Hkv = Hkv;
+  qp.d = d;
+  qp.eps = c.rms_eps;
+  qp.qk_norm = c.qk_norm;
+  qp.err = err;
+  qp.qkv = qkv;
+  qp.qkv_ld = QKV;
+  qp.kv_only = 0;
+  pallas::AttnParams ap;
+  ap.q = q;
+  ap.bt = bt;
+  ap.max_pages = max_pages;
+  ap.num_pages = pool->num_pages;
+  ap.page = pool->page_size;
+  ap.o = o;
+  ap.Hq = Hq;
+  ap.Hkv = Hkv;
+  ap.d = d;
+  ap.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(d)));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const pallas_layer_weights& L = m->layers[l];
+    const Planes pl = layer_planes(pool, l);
+    if (l > 0) PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.attn_norm), h, B, H, c.rms_eps, s), "rmsnorm");
+    PALLAS_TRY(project(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, B, QKV, H, s), "qkv proj");
+    qp.q_gain = u16(L.q_norm);
+    qp.k_gain = u16(L.k_norm);
+    qp.k_plane = pl.k;
+    qp.v_plane = pl.v;
+    PALLAS_TRY(pallas::launch_qkv_rope(qp, rm, B, s), "qkv epilogue");
+    ap.k_plane = pl.k;
+    ap.v_plane = pl.v;
+    PALLAS_TRY(pallas::launch_attention_decode(ap, rm, s), "decode attention");
+    PALLAS_TRY(project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, s), "o proj");
+    PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, B, H, c.rms_eps, s), "rmsnorm");
+    PALLAS_TRY(project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, s), "gate_up proj");
+    PALLAS_TRY(project(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, B, H, F, s), "down proj");
+  }
+  PALLAS_TRY(pallas::launch_rmsnorm(r, u16(m->final_norm), h, B, H, c.rms_eps, s), "final norm");
+  PALLAS_TRY(project(pallas::kEpiF32, h, H, u16(m->lm_head), H, logits, c.vocab, B, c.vocab, H, s), "lm_head");
+  return PALLAS_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t max_seqs) {
@@ -280,19 +481,59 @@ int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_to
                           const int32_t* h_cu_seqlens, const int32_t* d_block_tables,
                           int32_t max_pages, const pallas_kv_pool* pool, void* d_workspace,
                           size_t ws_bytes, int32_t* d_err, void* stream) {
-  (void)m; (void)num_seqs; (void)d_token_ids; (void)h_cu_seqlens; (void)d_block_tables;
-  (void)max_pages; (void)pool; (void)d_workspace; (void)ws_bytes; (void)d_err; (void)stream;
-  return fail(PALLAS_ERR_UNSUPPORTED, "prefill: not built yet");
+  if (!m) return fail(PALLAS_ERR_INVALID_ARG, "prefill: null model");
+  if (num_seqs < 1 || num_seqs > PALLAS_MAX_SEQS)
+    return fail(PALLAS_ERR_INVALID_ARG, "prefill: num_seqs %d outside [1, %d]", num_seqs, PALLAS_MAX_SEQS);
+  if (!d_token_ids || !h_cu_seqlens || !d_block_tables || max_pages <= 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "prefill: null ids, cu_seqlens or block tables");
+  if (int rc = check_model_pool(m, pool, "prefill")) return rc;
+  pallas::RowMap rm;
+  rm.n_seqs = num_seqs;
+  if (h_cu_seqlens[0] != 0) return fail(PALLAS_ERR_INVALID_ARG, "prefill: cu_seqlens[0] must be 0");
+  const int64_t cap = int64_t(max_pages) * pool->page_size;
+  for (int i = 0; i <= num_seqs; ++i) rm.cu[i] = h_cu_seqlens[i];
+  for (int i = 0; i < num_seqs; ++i) {
+    const int64_t len = int64_t(h_cu_seqlens[i + 1]) - h_cu_seqlens[i];
+    if (len < 1) return fail(PALLAS_ERR_INVALID_ARG, "prefill: sequence %d has length %lld", i, (long long)len);
+    if (len > cap)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "prefill: sequence %d of %lld tokens exceeds the table (%lld)", i,
+                  (long long)len, (long long)cap);
+    rm.base_pos[i] = 0;
+  }
+  const int64_t M = h_cu_seqlens[num_seqs];
+  if (M > (int64_t(1) << 24)) return fail(PALLAS_ERR_UNSUPPORTED, "prefill: too many tokens");
+  if (int rc = check_workspace(m, d_workspace, ws_bytes, M, "prefill")) return rc;
+  return run_prefill(m, rm, static_cast<int>(M), d_token_ids, d_block_tables, max_pages, pool,
+                     static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));
 }
 
 int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_tokens,
                        const int32_t* h_positions, const int32_t* d_block_tables,
                        int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,
                        void* d_workspace, size_t ws_bytes, int32_t* d_err, void* stream) {
-  (void)m; (void)num_seqs; (void)d_tokens; (void)h_positions; (void)d_block_tables;
-  (void)max_pages; (void)pool; (void)d_logits; (void)d_workspace; (void)ws_bytes; (void)d_err;
-  (void)stream;
-  return fail(PALLAS_ERR_UNSUPPORTED, "decode: not built yet");
+  if (!m) return fail(PALLAS_ERR_INVALID_ARG, "decode: null model");
+  if (num_seqs < 1 || num_seqs > PALLAS_MAX_SEQS)
+    return fail(PALLAS_ERR_INVALID_ARG, "decode: num_seqs %d outside [1, %d]", num_seqs, PALLAS_MAX_SEQS);
+  if (!d_tokens || !h_positions || !d_block_tables || !d_logits || max_pages <= 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "decode: null tokens, positions, tables or logits");
+  if (int rc = check_model_pool(m, pool, "decode")) return rc;
+  pallas::RowMap rm;
+  rm.n_seqs = num_seqs;
+  const int64_t cap = int64_t(max_pages) * pool->page_size;
+  for (int i = 0; i < num_seqs; ++i) {
+    rm.cu[i] = i;
+    const int n = h_positions[i];
+    if (n < 0 || int64_t(n) + 1 > cap)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "decode: position %d of sequence %d outside the table (%lld)", n, i,
+                  (long long)cap);
+    if (n >= kDecodeMaxPos)
+      return fail(PALLAS_ERR_UNSUPPORTED, "decode: position %d beyond %d", n, kDecodeMaxPos - 1);
+    rm.base_pos[i] = n;
+  }
+  rm.cu[num_seqs] = num_seqs;
+  if (int rc = check_workspace(m, d_workspace, ws_bytes, num_seqs, "decode")) return rc;
+  return run_decode(m, rm, d_tokens, d_block_tables, max_pages, pool, d_logits,
+                    static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

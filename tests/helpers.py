@@ -45,3 +45,34 @@ def make_headers(P, pieces, cfg_kv, req=1, epoch=1):
     """pieces: list of (start, count, arena_offset)."""
     L, hkv, d = cfg_kv
     return [P.ChunkHeader(req, epoch, s, c, off, L, hkv, d, 2) for s, c, off in pieces]
+
+
+# ------------------------------------------------------------ reconstruction
+def gpu_model(P, cfg, glob, layers, device="cuda"):
+    g = {k: v.to(device).contiguous() for k, v in glob.items()}
+    ls = [{k: v.to(device).contiguous() for k, v in l.items()} for l in layers]
+    return P.Model(cfg, g, ls)
+
+
+def empty_pool(cfg, pages, device="cuda", fill_bits=None):
+    shape = (cfg.n_layers, 2, pages, cfg.page_size, cfg.n_kv_heads, cfg.head_dim)
+    pool = torch.empty(shape, dtype=torch.bfloat16, device=device)
+    if fill_bits is not None:
+        pool.view(torch.int16).fill_(fill_bits)
+    return pool
+
+
+def kv_logical(pool: torch.Tensor, bt: np.ndarray, n: int) -> np.ndarray:
+    """[L, 2, n, Hkv, d] float64 values of positions [0, n) through table bt."""
+    page = pool.shape[3]
+    t = np.arange(n)
+    pages = torch.as_tensor(np.asarray(bt)[t // page], device=pool.device, dtype=torch.long)
+    slots = torch.as_tensor(t % page, device=pool.device, dtype=torch.long)
+    return pool[:, :, pages, slots].to(torch.float64).cpu().numpy()
+
+
+def rel_err(got: np.ndarray, ref: np.ndarray) -> float:
+    return float(np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-30))
+
+
+TOL = 1e-2   # max|gpu - ref| <= TOL * max|ref| per (layer, K|V) tensor and per logits row
