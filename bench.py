@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""Benchmark of target-side KV-cache reconstruction on one MI355X.
+
+One step is one pass of the whole reconstruction path over the workload:
+
+  1. prefix prefill of every request's prefix [0, p_i) into the target pool
+     (K/V written into 16-token pages through the target block tables);
+  2. pack of every request's suffix [p_i, n_i) out of the source pool into
+     contiguous per-layer transfer chunks;
+  3. assembly of those chunks into the target block tables;
+  4. one batched decode step at positions n_i over the assembled caches.
+
+Inputs are synthetic and resident in device memory before timing starts:
+random-init bf16 weights N(0, 0.02) of the workload's decoder shape, uniform
+token ids, shuffled block tables; the source pool holds the K/V of a
+source-side full prefill of [0, n_i) (run once, untimed).
+
+The printed JSON line reports prefix tokens per second over the whole step,
+the per-phase breakdown (prefill tokens/s and fraction of the bf16 MFMA
+peak, pack/assemble GB/s and fraction of the HBM peak), the roofline of the
+dominant kernel (the gate|up projection GEMM, timed with HIP events on the
+launch stream inside the timed region), and the CPU oracle timed on a
+bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+METRIC = "prefix-prefill tokens/s + % bf16 MFMA peak; KV pack/assemble GB/s + % HBM peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="large",
+                    choices=["tiny", "mid", "large", "large-aligned", "concurrent"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def load_library():
+    import paper_2608_16477_amd as P
+    if not os.path.exists(P.library_path()):
+        from paper_2608_16477_amd import build
+        build.build()
+    P.lib()
+    return P
+
+
+class Setup:
+    """Device-resident inputs of one workload."""
+
+    def __init__(self, P, wl, seed):
+        import numpy as np
+        import torch
+        from workloads import gen
+
+        self.P, self.wl, self.cfg = P, wl, wl.model
+        cfg, dev = self.cfg, "cuda"
+        self.glob, self.layers = gen.model_weights(cfg, seed=seed, device=dev)
+        self.model = P.Model(cfg, self.glob, self.layers)
+        B = wl.num_seqs
+        self.ns, self.ps = list(wl.ctx), list(wl.prefix)
+        self.ids = [gen.token_ids(n + 1, cfg.vocab, seed=seed, stream=i).numpy()
+                    for i, n in enumerate(self.ns)]
+        src_pages = [wl.pages_for(n) for n in self.ns]
+        dst_pages = [wl.pages_for(n + 1) for n in self.ns]
+        self.max_pages = max(dst_pages)
+        src_pool_pages, dst_pool_pages = sum(src_pages), sum(dst_pages)
+        self.src_tab = torch.tensor(gen.disjoint_block_tables(src_pages, src_pool_pages, self.max_pages,
+                                                              seed, 1), dtype=torch.int32, device=dev)
+        self.dst_tab = torch.tensor(gen.disjoint_block_tables(dst_pages, dst_pool_pages, self.max_pages,
+                                                              seed, 2), dtype=torch.int32, device=dev)
+        shape = (cfg.n_layers, 2, 0, cfg.page_size, cfg.n_kv_heads, cfg.head_dim)
+        self.src = torch.zeros(shape[:2] + (src_pool_pages,) + shape[3:], dtype=torch.bfloat16, device=dev)
+        self.dst = torch.zeros(shape[:2] + (dst_pool_pages,) + shape[3:], dtype=torch.bfloat16, device=dev)
+        self.err = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.prefix_ids = torch.tensor(np.concatenate([ids[:p] for ids, p in zip(self.ids, self.ps)]),
+                                       dtype=torch.int32, device=dev)
+        self.cu = [0]
+        for p in self.ps:
+            self.cu.append(self.cu[-1] + p)
+        self.tokens = torch.tensor([ids[n] for ids, n in zip(self.ids, self.ns)], dtype=torch.int32,
+                                   device=dev)
+        self.logits = torch.empty((B, cfg.vocab), dtype=torch.float32, device=dev)
+        self.ws = self.model.workspace(max(self.cu[-1], max(self.ns)), B)
+        # suffix chunks per request
+        row = 2 * cfg.n_layers * cfg.n_kv_heads * cfg.head_dim * 2
+        self.row_bytes = row
+        self.descs, self.hdrs = [], []
+        off = 0
+        for i, (n, p) in enumerate(zip(self.ns, self.ps)):
+            step = wl.chunk_tokens or (n - p)
+            d, h = [], []
+            for t in range(p, n, step):
+                c = min(step, n - t)
+                d.append(P.ChunkDesc(t, c, off))
+                h.append(P.ChunkHeader(1000 + i, 1, t, c, off, cfg.n_layers, cfg.n_kv_heads,
+                                       cfg.head_dim, 2))
+                off += c * row
+            self.descs.append(d)
+            self.hdrs.append(h)
+        self.arena = torch.empty(max(off, 16), dtype=torch.uint8, device=dev)
+        self.suffix_tokens = sum(n - p for n, p in zip(self.ns, self.ps))
+        # source cache: full prefill of [0, n_i), untimed
+        for i, n in enumerate(self.ns):
+            self.model.prefill_prefix(torch.tensor(self.ids[i][:n], dtype=torch.int32, device=dev), [0, n],
+                                      self.src_tab[i:i + 1], self.src, self.ws, self.err)
+        torch.cuda.synchronize()
+
+    def prefill(self):
+        self.model.prefill_prefix(self.prefix_ids, self.cu, self.dst_tab, self.dst, self.ws, self.err)
+
+    def pack(self):
+        for i in range(self.wl.num_seqs):
+            self.P.pallas_pack_suffix_blocks(self.src, self.src_tab[i], self.descs[i], self.arena, self.err)
+
+    def assemble(self):
+        for i in range(self.wl.num_seqs):
+            self.P.pallas_assemble_kv(self.dst, self.dst_tab[i], self.hdrs[i], self.arena, 1000 + i, 1,
+                                      self.err)
+
+    def decode(self):
+        self.model.decode_step(self.tokens, self.ns, self.dst_tab, self.dst, self.logits, self.ws, self.err)
+
+
+def cpu_baseline(setup):
+    """The oracle's first decoder layer (float64 numpy) over the workload's
+    prefix rows, scaled by the layer count; plus the oracle's pack of the
+    suffix from a host copy of the source pool."""
+    import numpy as np
+    import torch
+    from oracle import model as om
+    from oracle import paged
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [os.cpu_count() or 1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    cfg = setup.cfg
+    shp = om.Shape.of(cfg)
+    w = {k: v.to("cpu", torch.float64).numpy() for k, v in setup.layers[0].items()}
+    i0 = 0
+    p = setup.ps[i0]
+    ids = setup.ids[i0][:p]
+    r = setup.glob["embed"][torch.as_tensor(ids, dtype=torch.long, device="cuda")].to("cpu", torch.float64).numpy()
+    pos = np.arange(p)
+    t0 = time.perf_counter()
+    om.layer(r, pos, None, None, w, shp, om.bf16_round)
+    t_layer = time.perf_counter() - t0
+    tok_s = p / (t_layer * cfg.n_layers)
+    # pack of the first request's suffix
+    n = setup.ns[i0]
+    src = setup.src.view(torch.int16).cpu().numpy()
+    bt = setup.src_tab[i0].cpu().numpy()
+    t0 = time.perf_counter()
+    chunk = paged.pack(src, bt, p, n - p)
+    t_pack = time.perf_counter() - t0
+    del src
+    return {
+        "value": tok_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"oracle decoder layer 0 in float64 over the {p}-token prefix "
+                   f"({t_layer:.2f} s), scaled by {cfg.n_layers} layers"),
+        "pack_GBps": 2 * chunk.nbytes / t_pack / 1e9,
+        "pack_sample": f"oracle pack of the {n - p}-token suffix ({chunk.nbytes / 1e6:.0f} MB) on 1 thread",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(the reconstruction path runs on one GPU with no collectives).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from workloads import workload
+
+    P = load_library()
+    wl = workload(args.workload)
+    cfg = wl.model
+    print(f"[bench] workload {wl.name}: {cfg.n_layers} layers, hidden {cfg.hidden}, "
+          f"{cfg.n_q_heads}/{cfg.n_kv_heads} heads, d {cfg.head_dim}, ffn {cfg.ffn}, "
+          f"ctx {wl.ctx}, prefix {wl.prefix}", file=sys.stderr, flush=True)
+    t0 = time.time()
+    st = Setup(P, wl, args.seed)
+    print(f"[bench] setup {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    phases = ("prefill", "pack", "assemble", "decode")
+    fns = (st.prefill, st.pack, st.assemble, st.decode)
+
+    def step(ev=None):
+        for k, f in enumerate(fns):
+            if ev is not None:
+                ev[k].record(stream)
+            f()
+        if ev is not None:
+            ev[len(fns)].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    P.pallas_profile_reset()
+    P.pallas_profile_enable(["gemm_gate_up", "gemm_qkv", "gemm_o", "gemm_down", "attention",
+                             "qkv_epilogue", "rmsnorm", "pack", "assemble"])
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    prof = P.pallas_profile_read()
+    P.pallas_profile_enable([])
+    assert int(st.err.item()) == 0, "device-side error flag raised"
+
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    phase_ms = {ph: sum(evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)) / args.steps
+                for i, ph in enumerate(phases)}
+    prefix_tokens = sum(st.ps)
+    flops = sum(cfg.prefill_flops(p) for p in st.ps)
+    copy_bytes = 2 * st.suffix_tokens * cfg.s_kv     # read + write of the payload
+    value = prefix_tokens / (ms_step / 1e3)
+
+    gu_ms, gu_n = prof["gemm_gate_up"]
+    gu_avg_s = gu_ms / gu_n / 1e3
+    gu_flops = 2.0 * prefix_tokens * 2 * cfg.ffn * cfg.hidden
+    achieved = gu_flops / gu_avg_s / 1e12
+    kernels = {k: {"avg_us": v[0] / v[1] * 1e3, "launches_per_step": v[1] / args.steps}
+               for k, v in prof.items() if v[1]}
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: {cfg.n_layers}-layer decoder, hidden {cfg.hidden}, "
+                         f"{cfg.n_q_heads}/{cfg.n_kv_heads} heads, head_dim {cfg.head_dim}, "
+                         f"ffn {cfg.ffn}, vocab {cfg.vocab}, qk_norm {cfg.qk_norm}; "
+                         f"{wl.num_seqs} request(s), ctx {wl.ctx}, prefix {wl.prefix}, "
+                         f"suffix chunks of {wl.chunk_tokens or 'the whole suffix'} tokens, page 16"),
+            "step": "prefix prefill + suffix pack + assembly + one decode step",
+            "prefix_tokens": prefix_tokens,
+            "suffix_tokens": st.suffix_tokens,
+        },
+        "breakdown": {
+            "prefill_ms": phase_ms["prefill"],
+            "prefill_tokens_per_s": prefix_tokens / (phase_ms["prefill"] / 1e3),
+            "prefill_tflops": flops / (phase_ms["prefill"] / 1e3) / 1e12,
+            "prefill_mfma_frac": flops / (phase_ms["prefill"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+            "pack_ms": phase_ms["pack"],
+            "pack_GBps": copy_bytes / (phase_ms["pack"] / 1e3) / 1e9,
+            "pack_hbm_frac": copy_bytes / (phase_ms["pack"] / 1e3) / 1e9 / PEAK_HBM_GBPS,
+            "assemble_ms": phase_ms["assemble"],
+            "assemble_GBps": copy_bytes / (phase_ms["assemble"] / 1e3) / 1e9,
+            "assemble_hbm_frac": copy_bytes / (phase_ms["assemble"] / 1e3) / 1e9 / PEAK_HBM_GBPS,
+            "decode_ms": phase_ms["decode"],
+            "kernels": kernels,
+            "host_wall_s": wall,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "gemm_bf16_kernel<2> (gate|up projection + SwiGLU)",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": None,
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(st)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -232,6 +232,38 @@ int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_token
 int pallas_check_coverage(int32_t prefix_len, const int32_t* h_starts, const int32_t* h_lens,
                           int32_t n_ranges, int32_t n);
 
+/* Per-kernel timing (tracing).  Kernel classes of the calls above: */
+typedef enum {
+  PALLAS_K_EMBED = 0,      /* token embedding + first RMSNorm */
+  PALLAS_K_RMSNORM = 1,
+  PALLAS_K_ROPE_TABLE = 2,
+  PALLAS_K_GEMM_QKV = 3,   /* prefill Q|K|V projection (K|V only in the last layer) */
+  PALLAS_K_QKV_EPI = 4,    /* QK-norm, rotary, paged K/V store */
+  PALLAS_K_ATTN = 5,       /* prefill causal attention */
+  PALLAS_K_GEMM_O = 6,     /* prefill output projection + residual */
+  PALLAS_K_GEMM_GATE_UP = 7, /* prefill gate|up projection + SwiGLU */
+  PALLAS_K_GEMM_DOWN = 8,  /* prefill down projection + residual */
+  PALLAS_K_PACK = 9,
+  PALLAS_K_ASSEMBLE = 10,
+  PALLAS_K_DECODE_PROJ = 11, /* decode projections and lm_head */
+  PALLAS_K_DECODE_ATTN = 12,
+  PALLAS_K_COUNT = 13
+} pallas_kernel_class;
+
+/* Enable timing for the classes whose bit (1 << class) is set in
+ * class_mask (0 disables).  Each timed launch is bracketed by two HIP events
+ * recorded on the launch's stream; nothing else changes.  Process-wide. */
+void pallas_profile_enable(uint32_t class_mask);
+
+/* Wait for every recorded event pair, add its elapsed time to the class
+ * totals, and copy the totals since the last reset: ms[k] (milliseconds) and
+ * launches[k] for k < PALLAS_K_COUNT (host arrays of PALLAS_K_COUNT entries;
+ * either may be NULL).  Returns PALLAS_ERR_HIP if an event query fails. */
+int pallas_profile_read(double* ms, int64_t* launches);
+
+/* Zero the class totals and drop pending event pairs. */
+void pallas_profile_reset(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -88,7 +88,14 @@ EXPORTS = {
     "pallas_decode_step": (C.c_int, [_vp, _i32, _vp, _pi32, _vp, _i32, C.POINTER(KVPoolC), _vp,
                                      _vp, _sz, _vp, _vp]),
     "pallas_check_coverage": (C.c_int, [_i32, _pi32, _pi32, _i32, _i32]),
+    "pallas_profile_enable": (None, [C.c_uint32]),
+    "pallas_profile_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
+    "pallas_profile_reset": (None, []),
 }
+
+KERNEL_CLASSES = ("embed", "rmsnorm", "rope_table", "gemm_qkv", "qkv_epilogue", "attention",
+                  "gemm_o", "gemm_gate_up", "gemm_down", "pack", "assemble", "decode_proj",
+                  "decode_attention")
 
 _LIB = None
 
@@ -217,6 +224,27 @@ def pallas_decode_step(h, tokens, positions: Sequence[int], block_tables, pool, 
                                     _ptr(logits), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _ptr(err),
                                     _stream(stream)))
+
+
+def pallas_profile_enable(classes=KERNEL_CLASSES):
+    """Time every launch of the named kernel classes (empty: disable)."""
+    mask = 0
+    for c in classes:
+        mask |= 1 << KERNEL_CLASSES.index(c)
+    lib().pallas_profile_enable(mask)
+
+
+def pallas_profile_reset():
+    lib().pallas_profile_reset()
+
+
+def pallas_profile_read():
+    """{class: (total_ms, launches)} since the last reset."""
+    n = len(KERNEL_CLASSES)
+    ms = (C.c_double * n)()
+    cnt = (C.c_int64 * n)()
+    _check(lib().pallas_profile_read(ms, cnt))
+    return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNEL_CLASSES)}
 
 
 class Model:

@@ -13,8 +13,10 @@
 // Softmax runs in fp32 in the log2 domain (scores pre-scaled by
 // log2(e)/sqrt(d)); P is rounded to bf16 for the PV product.
 //
-// Decode: one workgroup per (sequence, query head): scores of the n+1 keys
-// into LDS, block max and sum, then the weighted sum of V rows.
+// Decode: split over keys (256 per workgroup, all query heads of one KV
+// head per workgroup), then a combine pass over the splits.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -189,75 +191,145 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(AttnParams p, RowMap 
 }
 
 constexpr int kDecThreads = 256;
-constexpr int kDecMaxKeys = 16384;
+constexpr int kDecSplit = 256;  // keys per split (one key per thread in the score pass)
+constexpr int kMaxG = 8;
 
+// Decode attention, split over keys: workgroup (seq, KV head, split) scores
+// its 256 keys for all G query heads of the KV head (each K row is read
+// once), keeps the split's max, sum and unnormalised output per head in the
+// partial buffer; decode_combine merges the splits.
 template <int D>
-__global__ __launch_bounds__(kDecThreads) void attn_decode_kernel(AttnParams p, RowMap rm) {
-  __shared__ float sc[kDecMaxKeys];
-  __shared__ float qs[D];
-  __shared__ float red[kDecThreads];
-  const int s = blockIdx.x / p.Hq, h = blockIdx.x % p.Hq;
-  const int G = p.Hq / p.Hkv, kh = h / G;
-  const int n = rm.base_pos[s];  // this token's position; keys [0, n]
+__global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnParams p, RowMap rm,
+                                                                        float* __restrict__ part,
+                                                                        int max_splits) {
+  __shared__ float qs[kMaxG][D];
+  __shared__ float sc[kMaxG][kDecSplit];
+  __shared__ float red[kMaxG][kDecThreads / 64];
+  __shared__ float oacc[kDecThreads / D][kMaxG][D];
+  const int G = p.Hq / p.Hkv;
+  const int split = blockIdx.x, kh = blockIdx.y, s = blockIdx.z;
+  const int n = rm.base_pos[s];
+  const int j0 = split * kDecSplit;
+  if (j0 > n) return;
+  const int jn = min(n + 1 - j0, kDecSplit);
   const int row = rm.cu[s];
   const int32_t* bt = p.bt + static_cast<int64_t>(s) * p.max_pages;
-  const uint16_t* q = p.q + (static_cast<int64_t>(row) * p.Hq + h) * D;
-  for (int i = threadIdx.x; i < D; i += kDecThreads) qs[i] = bf2f(q[i]);
+  for (int i = threadIdx.x; i < G * D; i += kDecThreads)
+    qs[i / D][i % D] = bf2f(p.q[(static_cast<int64_t>(row) * p.Hq + kh * G + i / D) * D + i % D]);
   __syncthreads();
 
-  float mx = -INFINITY;
-  for (int j = threadIdx.x; j <= n; j += kDecThreads) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float sv[kMaxG];
+#pragma unroll
+  for (int g = 0; g < kMaxG; ++g) sv[g] = -INFINITY;
+  if (threadIdx.x < jn) {
+    const int j = j0 + threadIdx.x;
     const int pg = bt[j / p.page];
-    float v = -INFINITY;
     if (pg >= 0 && pg < p.num_pages) {
       const uint16_t* k = p.k_plane + ((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D;
-      float acc = 0.f;
+      float acc[kMaxG];
 #pragma unroll
+      for (int g = 0; g < kMaxG; ++g) acc[g] = 0.f;
+#pragma unroll 4
       for (int c = 0; c < D / 8; ++c) {
         const u32x4 w = *reinterpret_cast<const u32x4*>(k + c * 8);
+        float kf[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          acc += qs[c * 8 + 2 * e] * bflo(w[e]) + qs[c * 8 + 2 * e + 1] * bfhi(w[e]);
+        for (int e = 0; e < 4; ++e) {
+          kf[2 * e] = bflo(w[e]);
+          kf[2 * e + 1] = bfhi(w[e]);
+        }
+#pragma unroll
+        for (int g = 0; g < kMaxG; ++g) {
+          if (g < G) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[g] += qs[g][c * 8 + e] * kf[e];
+          }
+        }
       }
-      v = acc * p.scale_log2;
+#pragma unroll
+      for (int g = 0; g < kMaxG; ++g) sv[g] = acc[g] * p.scale_log2;
     }
-    sc[j] = v;
-    mx = fmaxf(mx, v);
   }
-  mx = wave_max(mx);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  __syncthreads();
-  float sum = 0.f;
-  for (int j = threadIdx.x; j <= n; j += kDecThreads) {
-    const float e = exp2f(sc[j] - mx);
-    sc[j] = e;
-    sum += e;
+  // per-head max over the split
+#pragma unroll
+  for (int g = 0; g < kMaxG; ++g) {
+    if (g >= G) break;
+    const float m = wave_max(sv[g]);
+    if (lane == 0) red[g][wave] = m;
   }
-  sum = wave_sum(sum);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sum;
   __syncthreads();
-  sum = red[0] + red[1] + red[2] + red[3];
+  float mx[kMaxG];
+#pragma unroll
+  for (int g = 0; g < kMaxG; ++g) {
+    mx[g] = -INFINITY;
+    if (g < G)
+      for (int w = 0; w < kDecThreads / 64; ++w) mx[g] = fmaxf(mx[g], red[g][w]);
+  }
   __syncthreads();
-
-  constexpr int NG = kDecThreads / D;  // key groups
+#pragma unroll
+  for (int g = 0; g < kMaxG; ++g) {
+    if (g >= G) break;
+    const float e = (mx[g] == -INFINITY) ? 0.f : exp2f(sv[g] - mx[g]);
+    sc[g][threadIdx.x] = e;
+    const float t = wave_sum(e);
+    if (lane == 0) red[g][wave] = t;
+  }
+  __syncthreads();
+  // weighted sum of V: thread (key group kg, dim dv)
+  constexpr int NG = kDecThreads / D;
   const int dv = threadIdx.x % D, kg = threadIdx.x / D;
-  float acc = 0.f;
-  for (int j = kg; j <= n; j += NG) {
+  float o[kMaxG];
+#pragma unroll
+  for (int g = 0; g < kMaxG; ++g) o[g] = 0.f;
+  for (int jj = kg; jj < jn; jj += NG) {
+    const int j = j0 + jj;
     const int pg = bt[j / p.page];
     if (pg < 0 || pg >= p.num_pages) continue;
-    const uint16_t* v = p.v_plane + ((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D;
-    acc += sc[j] * bf2f(v[dv]);
+    const float v = bf2f(p.v_plane[((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D + dv]);
+#pragma unroll
+    for (int g = 0; g < kMaxG; ++g)
+      if (g < G) o[g] += sc[g][jj] * v;
   }
-  red[threadIdx.x] = acc;
+#pragma unroll
+  for (int g = 0; g < kMaxG; ++g)
+    if (g < G) oacc[kg][g][dv] = o[g];
   __syncthreads();
-  if (kg == 0) {
+  // partial record per (seq, head, split): [max, sum, o[0..D)]
+  for (int i = threadIdx.x; i < G * D; i += kDecThreads) {
+    const int g = i / D, e = i % D;
     float t = 0.f;
 #pragma unroll
-    for (int i = 0; i < NG; ++i) t += red[i * D + dv];
-    p.o[(static_cast<int64_t>(row) * p.Hq + h) * D + dv] = f2bf(t / sum);
+    for (int q = 0; q < NG; ++q) t += oacc[q][g][e];
+    float* rec = part + ((static_cast<int64_t>(s) * p.Hq + kh * G + g) * max_splits + split) * (D + 2);
+    rec[2 + e] = t;
+    if (e == 0) {
+      float sum = 0.f;
+      for (int w = 0; w < kDecThreads / 64; ++w) sum += red[g][w];
+      rec[0] = mx[g];
+      rec[1] = sum;
+    }
   }
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnParams p, RowMap rm,
+                                                                const float* __restrict__ part,
+                                                                int max_splits) {
+  const int h = blockIdx.x, s = blockIdx.y;
+  const int n = rm.base_pos[s];
+  const int nsplit = n / kDecSplit + 1;
+  const float* base = part + (static_cast<int64_t>(s) * p.Hq + h) * max_splits * (D + 2);
+  float m = -INFINITY;
+  for (int k = 0; k < nsplit; ++k) m = fmaxf(m, base[k * (D + 2)]);
+  float l = 0.f, o = 0.f;
+  for (int k = 0; k < nsplit; ++k) {
+    const float* rec = base + k * (D + 2);
+    const float w = (rec[0] == -INFINITY) ? 0.f : exp2f(rec[0] - m);
+    l += w * rec[1];
+    o += w * rec[2 + threadIdx.x];
+  }
+  p.o[(static_cast<int64_t>(rm.cu[s]) * p.Hq + h) * D + threadIdx.x] = f2bf(l > 0.f ? o / l : 0.f);
 }
 
 }  // namespace
@@ -282,16 +354,26 @@ hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipSt
   return hipGetLastError();
 }
 
-hipError_t launch_attention_decode(const AttnParams& p, const RowMap& rm, hipStream_t s) {
-  for (int i = 0; i < rm.n_seqs; ++i)
-    if (rm.base_pos[i] < 0 || rm.base_pos[i] >= kDecMaxKeys) return hipErrorInvalidValue;
-  const int blocks = rm.n_seqs * p.Hq;
-  if (p.d == 128)
-    attn_decode_kernel<128><<<blocks, kDecThreads, 0, s>>>(p, rm);
-  else if (p.d == 64)
-    attn_decode_kernel<64><<<blocks, kDecThreads, 0, s>>>(p, rm);
-  else
+hipError_t launch_attention_decode(const AttnParams& p, const RowMap& rm, float* partial,
+                                   int max_splits, hipStream_t s) {
+  int nmax = 0;
+  for (int i = 0; i < rm.n_seqs; ++i) {
+    if (rm.base_pos[i] < 0) return hipErrorInvalidValue;
+    nmax = std::max(nmax, rm.base_pos[i]);
+  }
+  const int splits = nmax / kDecSplit + 1;
+  if (splits > max_splits || p.Hq / p.Hkv > kMaxG) return hipErrorInvalidValue;
+  dim3 grid(splits, p.Hkv, rm.n_seqs);
+  dim3 cgrid(p.Hq, rm.n_seqs);
+  if (p.d == 128) {
+    attn_decode_split_kernel<128><<<grid, kDecThreads, 0, s>>>(p, rm, partial, max_splits);
+    attn_decode_combine_kernel<128><<<cgrid, 128, 0, s>>>(p, rm, partial, max_splits);
+  } else if (p.d == 64) {
+    attn_decode_split_kernel<64><<<grid, kDecThreads, 0, s>>>(p, rm, partial, max_splits);
+    attn_decode_combine_kernel<64><<<cgrid, 64, 0, s>>>(p, rm, partial, max_splits);
+  } else {
     return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

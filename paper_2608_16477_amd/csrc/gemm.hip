@@ -3,17 +3,19 @@
 // accumulator, with the epilogue fused into the store.
 //
 // Tiling: a 256 x 256 output tile per workgroup of 4 waves, each wave
-// 128 x 128 as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at
-// a time through a double-buffered LDS stage (2 x (32 KiB A + 32 KiB B))
-// filled by buffer loads that write LDS directly (no register staging); the
-// buffer range check turns rows past M/N and columns past K into zeros.
-// LDS rows are 8 chunks of 16 bytes with the chunk index XOR-swizzled by
-// (row / 2) mod 8, so the 16-byte fragment reads of 16 consecutive rows hit
-// 16 distinct 4-bank groups.
+// 128 x 128 as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.  K advances 32 at
+// a time through a 4-deep LDS ring (4 x (16 KiB A + 16 KiB B)) filled by
+// buffer loads that write LDS directly (no register staging), issued three
+// K-steps ahead of the math so HBM latency hides behind three steps of
+// MFMA work; one barrier per step.  The buffer range check turns rows past
+// M/N and columns past K into zeros.
 //
 // Workgroups are dispatched round-robin over the 8 XCDs; the tile index is
 // remapped so each XCD owns a contiguous run of tiles, M-tile fastest, so
 // the workgroups sharing one weight panel run on one XCD and share its L2.
+#include <algorithm>
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -21,23 +23,29 @@ namespace pallas {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int kStages = 5;               // LDS ring depth (5 x 32 KiB = all of LDS)
 constexpr int kThreads = 256;
 constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
 constexpr int kSlots = BM * kChunks;     // 16-byte slots per operand tile
+constexpr int kLoads = kSlots / kThreads;  // load instructions per thread per operand
 constexpr int kXcds = 8;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-__device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 7)); }
+// 64-byte rows: four rows span the 64 banks; XOR the chunk with (row / 4)
+// mod 4 so 16 consecutive rows read at one logical chunk hit 16 distinct
+// 4-bank groups.
+__device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 2) & 3)); }
 
 __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
                                               const int* row_off_valid, const int* chunk, int k0,
                                               int K, u32x4* lds_tile, int wave, int lane) {
-  // 8 instructions per wave; instruction i fills slots [(wave*8+i)*64, +64).
+  // kLoads instructions per wave; instruction i fills slots
+  // [(wave*kLoads+i)*64, +64).
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int base = (wave * 8 + i) * 64;
+  for (int i = 0; i < kLoads; ++i) {
+    const int base = (wave * kLoads + i) * 64;
     const int k = k0 + chunk[i] * 8;
     const uint32_t off = (row_off_valid[i] >= 0 && k < K)
                              ? static_cast<uint32_t>(row_off_valid[i]) + static_cast<uint32_t>(k) * 2u
@@ -49,7 +57,7 @@ __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint3
 
 template <int EPI>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) u32x4 lds[2][2][kSlots];  // [buf][A|B][slot]
+  __shared__ __attribute__((aligned(16))) u32x4 lds[kStages][2][kSlots];  // [stage][A|B][slot]
 
   const int bid = blockIdx.x;
   const int loc = bid / kXcds;
@@ -65,12 +73,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
 
   // Per-thread load plan: row byte offsets (or -1 when out of range) and
   // source chunk of the LDS slot each load instruction fills.
-  int a_off[8], b_off[8], chunk[8];
+  int a_off[kLoads], b_off[kLoads], chunk[kLoads];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int s = (wave * 8 + i) * 64 + lane;
+  for (int i = 0; i < kLoads; ++i) {
+    const int s = (wave * kLoads + i) * 64 + lane;
     const int row = s / kChunks;
-    chunk[i] = (s % kChunks) ^ ((row >> 1) & 7);
+    chunk[i] = (s % kChunks) ^ ((row >> 2) & 3);
     const int gm = m0 + row;
     a_off[i] = gm < p.M ? gm * p.lda * 2 : -1;
     int gn;
@@ -105,36 +113,77 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     brow[j] = (EPI == kEpiSwiGLU ? (j >> 1) * 128 + wn * 64 + (j & 1) * 32 : wn * 128 + j * 32) + l32;
 
   const int KT = (p.K + BK - 1) / BK;
-  load_tile_lds(ra, p.a_bytes, a_off, chunk, 0, p.K, lds[0][0], wave, lane);
-  load_tile_lds(rb, p.b_bytes, b_off, chunk, 0, p.K, lds[0][1], wave, lane);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) {
-      load_tile_lds(ra, p.a_bytes, a_off, chunk, (kt + 1) * BK, p.K, lds[buf ^ 1][0], wave, lane);
-      load_tile_lds(rb, p.b_bytes, b_off, chunk, (kt + 1) * BK, p.K, lds[buf ^ 1][1], wave, lane);
+  // Prologue: stages 0 .. kStages-2 in flight; then stage 0 resident.
+#pragma unroll
+  for (int st = 0; st < kStages - 1; ++st) {
+    if (st < KT) {
+      load_tile_lds(ra, p.a_bytes, a_off, chunk, st * BK, p.K, lds[st][0], wave, lane);
+      load_tile_lds(rb, p.b_bytes, b_off, chunk, st * BK, p.K, lds[st][1], wave, lane);
     }
-    const u32x4* At = lds[buf][0];
-    const u32x4* Bt = lds[buf][1];
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int c = kk * 2 + g;
-      bf16x8 a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = __builtin_bit_cast(bf16x8, At[swz(arow[i], c)]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
   }
+  if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads * (kStages - 2)) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+
+  // Fragment registers: [k-half][block]; half 0 of step kt is read during
+  // step kt-1, half 1 during the first half of step kt.
+  bf16x8 fa[2][4], fb[2][4];
+  auto read_frags = [&](int slot, int kk, bf16x8* a, bf16x8* b) {
+    const u32x4* At = lds[slot][0];
+    const u32x4* Bt = lds[slot][1];
+    const int c = kk * 2 + g;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = __builtin_bit_cast(bf16x8, At[swz(arow[i], c)]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
+  };
+  auto mfma_block = [&](const bf16x8* a, const bf16x8* b) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  };
+  read_frags(0, 0, fa[0], fb[0]);
+
+  // One K-step: refill the slot of step kt-1 (kRefill), MFMAs on half 0
+  // while half 1 is read, wait for stage kt+1 and barrier, MFMAs on half 1
+  // while half 0 of step kt+1 is read.  The steady loop has no branches so
+  // the LDS reads interleave with the MFMAs.
+  auto step = [&](int kt, auto refill_tag) {
+    constexpr bool kRefill = decltype(refill_tag)::value;
+    const int slot = kt % kStages;
+    if (kRefill) {
+      const int nk = kt + kStages - 1;
+      const int ns = nk % kStages;
+      load_tile_lds(ra, p.a_bytes, a_off, chunk, nk * BK, p.K, lds[ns][0], wave, lane);
+      load_tile_lds(rb, p.b_bytes, b_off, chunk, nk * BK, p.K, lds[ns][1], wave, lane);
+    }
+    read_frags(slot, 1, fa[1], fb[1]);
+    mfma_block(fa[0], fb[0]);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+    }
+    if (kRefill)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads * (kStages - 2)) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    // Step kt+1 is resident; its slot index is valid even past the end
+    // (the fragments are then unused).
+    read_frags((kt + 1) % kStages, 0, fa[0], fb[0]);
+    mfma_block(fa[1], fb[1]);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+  };
+  int kt = 0;
+  for (; kt + kStages - 1 < KT; ++kt) step(kt, std::true_type{});
+  for (; kt < KT; ++kt) step(kt, std::false_type{});
 
   // Epilogue.  Accumulator register r of block (i, j) holds
   // row wm*128 + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.

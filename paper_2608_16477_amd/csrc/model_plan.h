@@ -20,10 +20,15 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Workspace carve-up for `tokens` rows (prefill: sum of prefix lengths;
 // decode: number of sequences).
 struct Workspace {
-  size_t resid, h, qkv, q, o, act, rope, total;
+  size_t resid, h, qkv, q, o, act, rope, part, total;
 };
 
-inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens) {
+// Decode positions are below this bound; decode attention keeps one partial
+// record per 256-key split.
+constexpr int kDecodeMaxPos = 16384;
+constexpr int kDecodeMaxSplits = kDecodeMaxPos / 256;
+
+inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens, int64_t seqs) {
   Workspace w;
   const int64_t qkv = int64_t(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
   size_t at = 0;
@@ -35,13 +40,13 @@ inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens) 
   w.o = take(size_t(tokens) * c.n_q_heads * c.head_dim * 2);
   w.act = take(size_t(tokens) * c.ffn * 2);
   w.rope = take(size_t(tokens) * (c.head_dim / 2) * 8);  // (cos, sin) per row and pair
+  w.part = take(size_t(seqs) * c.n_q_heads * kDecodeMaxSplits * (c.head_dim + 2) * 4);
   w.total = at;
   return w;
 }
 
 inline size_t workspace_bytes(const pallas_model_config& c, int32_t max_tokens, int32_t max_seqs) {
-  (void)max_seqs;
-  return workspace_layout(c, max_tokens).total;
+  return workspace_layout(c, max_tokens, max_seqs).total;
 }
 
 }  // namespace pallas

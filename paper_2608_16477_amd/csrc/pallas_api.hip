@@ -12,6 +12,7 @@
 #include "pallas.h"
 #include "kernels.h"
 #include "model_plan.h"
+#include "profile.h"
 
 namespace {
 
@@ -81,6 +82,7 @@ int run_copies(bool pack, const pallas::PoolGeom& g, const int32_t* bt, char* ar
       b.n += 1;
       b.unit_prefix[b.n] = static_cast<int32_t>(units);
     }
+    pallas::ProfScope ps(pack ? PALLAS_K_PACK : PALLAS_K_ASSEMBLE, s);
     hipError_t e = pallas::launch_kv_copy(pack, g, bt, arena, b, d_err, s);
     if (e != hipSuccess) return hip_fail(e, pack ? "pack launch" : "assemble launch");
   }
@@ -272,8 +274,6 @@ void pallas_model_destroy(pallas_model* m) { delete m; }
 // ------------------------------------------------------------- prefill / decode
 namespace {
 
-constexpr int kDecodeMaxPos = 16384;
-
 int check_model_pool(const pallas_model* m, const pallas_kv_pool* pool, const char* what) {
   if (int rc = check_pool(pool, what)) return rc;
   const pallas_model_config& c = m->cfg;
@@ -283,18 +283,20 @@ int check_model_pool(const pallas_model* m, const pallas_kv_pool* pool, const ch
   return PALLAS_OK;
 }
 
-int check_workspace(const pallas_model* m, const void* ws, size_t bytes, int64_t rows, const char* what) {
+int check_workspace(const pallas_model* m, const void* ws, size_t bytes, int64_t rows, int64_t seqs,
+                    const char* what) {
   if (!ws) return fail(PALLAS_ERR_INVALID_ARG, "%s: null workspace", what);
   if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0)
     return fail(PALLAS_ERR_INVALID_ARG, "%s: workspace not 256-byte aligned", what);
-  const size_t need = pallas::workspace_layout(m->cfg, rows).total;
+  const size_t need = pallas::workspace_layout(m->cfg, rows, seqs).total;
   if (bytes < need)
     return fail(PALLAS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", what, bytes, need);
   return PALLAS_OK;
 }
 
-#define PALLAS_TRY(expr, where)                       \
+#define PALLAS_TRY(cls, expr, where)                  \
   do {                                                \
+    pallas::ProfScope ps_(cls, s);                    \
     hipError_t e_ = (expr);                           \
     if (e_ != hipSuccess) return hip_fail(e_, where); \
   } while (0)
@@ -324,7 +326,7 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
                 const int32_t* bt, int max_pages, const pallas_kv_pool* pool, char* ws, int32_t* err,
                 hipStream_t s) {
   const pallas_model_config& c = m->cfg;
-  const pallas::Workspace w = pallas::workspace_layout(c, M);
+  const pallas::Workspace w = pallas::workspace_layout(c, M, rm.n_seqs);
   float* r = reinterpret_cast<float*>(ws + w.resid);
   uint16_t* h = reinterpret_cast<uint16_t*>(ws + w.h);
   uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + w.qkv);
@@ -335,8 +337,8 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
   const int H = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int QKV = (Hq + 2 * Hkv) * d, QD = Hq * d, KVD = 2 * Hkv * d;
 
-  PALLAS_TRY(pallas::launch_rope_table(rm, M, d, c.rope_theta, rope, s), "rope table");
-  PALLAS_TRY(pallas::launch_embed_rmsnorm(ids, u16(m->embed), u16(m->layers[0].attn_norm), r, h, M, H,
+  PALLAS_TRY(PALLAS_K_ROPE_TABLE, pallas::launch_rope_table(rm, M, d, c.rope_theta, rope, s), "rope table");
+  PALLAS_TRY(PALLAS_K_EMBED, pallas::launch_embed_rmsnorm(ids, u16(m->embed), u16(m->layers[0].attn_norm), r, h, M, H,
                                           c.rms_eps, c.vocab, err, s), "embed");
   pallas::QkvParams qp;
   qp.rope = rope;
@@ -367,34 +369,34 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
     const pallas_layer_weights& L = m->layers[l];
     const bool last = l == c.n_layers - 1;
     const Planes pl = layer_planes(pool, l);
-    if (l > 0) PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.attn_norm), h, M, H, c.rms_eps, s), "rmsnorm");
+    if (l > 0) PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.attn_norm), h, M, H, c.rms_eps, s), "rmsnorm");
     qp.q_gain = u16(L.q_norm);
     qp.k_gain = u16(L.k_norm);
     qp.k_plane = pl.k;
     qp.v_plane = pl.v;
     if (last) {
       // Only K and V of the last layer reach the cache.
-      PALLAS_TRY(pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv) + int64_t(QD) * H, H, qkv, KVD, M,
+      PALLAS_TRY(PALLAS_K_GEMM_QKV, pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv) + int64_t(QD) * H, H, qkv, KVD, M,
                                      KVD, H, s), "kv gemm");
       qp.qkv = qkv;
       qp.qkv_ld = KVD;
       qp.kv_only = 1;
-      PALLAS_TRY(pallas::launch_qkv_rope(qp, rm, M, s), "kv epilogue");
+      PALLAS_TRY(PALLAS_K_QKV_EPI, pallas::launch_qkv_rope(qp, rm, M, s), "kv epilogue");
       break;
     }
-    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, M, QKV, H, s), "qkv gemm");
+    PALLAS_TRY(PALLAS_K_GEMM_QKV, pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, M, QKV, H, s), "qkv gemm");
     qp.qkv = qkv;
     qp.qkv_ld = QKV;
     qp.kv_only = 0;
-    PALLAS_TRY(pallas::launch_qkv_rope(qp, rm, M, s), "qkv epilogue");
+    PALLAS_TRY(PALLAS_K_QKV_EPI, pallas::launch_qkv_rope(qp, rm, M, s), "qkv epilogue");
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
-    PALLAS_TRY(pallas::launch_attention_prefill(ap, rm, s), "attention");
-    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, s), "o gemm");
-    PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, M, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, M, F, H, s),
+    PALLAS_TRY(PALLAS_K_ATTN, pallas::launch_attention_prefill(ap, rm, s), "attention");
+    PALLAS_TRY(PALLAS_K_GEMM_O, pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, s), "o gemm");
+    PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, M, H, c.rms_eps, s), "rmsnorm");
+    PALLAS_TRY(PALLAS_K_GEMM_GATE_UP, pallas::launch_gemm(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, M, F, H, s),
                "gate_up gemm");
-    PALLAS_TRY(pallas::launch_gemm(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, M, H, F, s), "down gemm");
+    PALLAS_TRY(PALLAS_K_GEMM_DOWN, pallas::launch_gemm(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, M, H, F, s), "down gemm");
   }
   return PALLAS_OK;
 }
@@ -404,7 +406,8 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
                hipStream_t s) {
   const pallas_model_config& c = m->cfg;
   const int B = rm.n_seqs;
-  const pallas::Workspace w = pallas::workspace_layout(c, B);
+  const pallas::Workspace w = pallas::workspace_layout(c, B, B);
+  float* part = reinterpret_cast<float*>(ws + w.part);
   float* r = reinterpret_cast<float*>(ws + w.resid);
   uint16_t* h = reinterpret_cast<uint16_t*>(ws + w.h);
   uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + w.qkv);
@@ -415,8 +418,8 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
   const int H = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int QKV = (Hq + 2 * Hkv) * d, QD = Hq * d;
 
-  PALLAS_TRY(pallas::launch_rope_table(rm, B, d, c.rope_theta, rope, s), "rope table");
-  PALLAS_TRY(pallas::launch_embed_rmsnorm(tokens, u16(m->embed), u16(m->layers[0].attn_norm), r, h, B, H,
+  PALLAS_TRY(PALLAS_K_ROPE_TABLE, pallas::launch_rope_table(rm, B, d, c.rope_theta, rope, s), "rope table");
+  PALLAS_TRY(PALLAS_K_EMBED, pallas::launch_embed_rmsnorm(tokens, u16(m->embed), u16(m->layers[0].attn_norm), r, h, B, H,
                                           c.rms_eps, c.vocab, err, s), "embed");
   pallas::QkvParams qp;
   qp.rope = rope;
@@ -448,23 +451,23 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
   for (int l = 0; l < c.n_layers; ++l) {
     const pallas_layer_weights& L = m->layers[l];
     const Planes pl = layer_planes(pool, l);
-    if (l > 0) PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.attn_norm), h, B, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(project(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, B, QKV, H, s), "qkv proj");
+    if (l > 0) PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.attn_norm), h, B, H, c.rms_eps, s), "rmsnorm");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, B, QKV, H, s), "qkv proj");
     qp.q_gain = u16(L.q_norm);
     qp.k_gain = u16(L.k_norm);
     qp.k_plane = pl.k;
     qp.v_plane = pl.v;
-    PALLAS_TRY(pallas::launch_qkv_rope(qp, rm, B, s), "qkv epilogue");
+    PALLAS_TRY(PALLAS_K_QKV_EPI, pallas::launch_qkv_rope(qp, rm, B, s), "qkv epilogue");
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
-    PALLAS_TRY(pallas::launch_attention_decode(ap, rm, s), "decode attention");
-    PALLAS_TRY(project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, s), "o proj");
-    PALLAS_TRY(pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, B, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, s), "gate_up proj");
-    PALLAS_TRY(project(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, B, H, F, s), "down proj");
+    PALLAS_TRY(PALLAS_K_DECODE_ATTN, pallas::launch_attention_decode(ap, rm, part, pallas::kDecodeMaxSplits, s), "decode attention");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, s), "o proj");
+    PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, B, H, c.rms_eps, s), "rmsnorm");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, s), "gate_up proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, B, H, F, s), "down proj");
   }
-  PALLAS_TRY(pallas::launch_rmsnorm(r, u16(m->final_norm), h, B, H, c.rms_eps, s), "final norm");
-  PALLAS_TRY(project(pallas::kEpiF32, h, H, u16(m->lm_head), H, logits, c.vocab, B, c.vocab, H, s), "lm_head");
+  PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(m->final_norm), h, B, H, c.rms_eps, s), "final norm");
+  PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiF32, h, H, u16(m->lm_head), H, logits, c.vocab, B, c.vocab, H, s), "lm_head");
   return PALLAS_OK;
 }
 
@@ -502,7 +505,7 @@ int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_to
   }
   const int64_t M = h_cu_seqlens[num_seqs];
   if (M > (int64_t(1) << 24)) return fail(PALLAS_ERR_UNSUPPORTED, "prefill: too many tokens");
-  if (int rc = check_workspace(m, d_workspace, ws_bytes, M, "prefill")) return rc;
+  if (int rc = check_workspace(m, d_workspace, ws_bytes, M, num_seqs, "prefill")) return rc;
   return run_prefill(m, rm, static_cast<int>(M), d_token_ids, d_block_tables, max_pages, pool,
                      static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));
 }
@@ -526,12 +529,12 @@ int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_token
     if (n < 0 || int64_t(n) + 1 > cap)
       return fail(PALLAS_ERR_OUT_OF_RANGE, "decode: position %d of sequence %d outside the table (%lld)", n, i,
                   (long long)cap);
-    if (n >= kDecodeMaxPos)
-      return fail(PALLAS_ERR_UNSUPPORTED, "decode: position %d beyond %d", n, kDecodeMaxPos - 1);
+    if (n >= pallas::kDecodeMaxPos)
+      return fail(PALLAS_ERR_UNSUPPORTED, "decode: position %d beyond %d", n, pallas::kDecodeMaxPos - 1);
     rm.base_pos[i] = n;
   }
   rm.cu[num_seqs] = num_seqs;
-  if (int rc = check_workspace(m, d_workspace, ws_bytes, num_seqs, "decode")) return rc;
+  if (int rc = check_workspace(m, d_workspace, ws_bytes, num_seqs, num_seqs, "decode")) return rc;
   return run_decode(m, rm, d_tokens, d_block_tables, max_pages, pool, d_logits,
                     static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));
 }
