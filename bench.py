@@ -217,8 +217,7 @@ def main():
     print("[bench] warmup done", file=sys.stderr, flush=True)
 
     P.pallas_profile_reset()
-    P.pallas_profile_enable(["gemm_gate_up", "gemm_qkv", "gemm_o", "gemm_down", "attention",
-                             "qkv_epilogue", "rmsnorm", "pack", "assemble"])
+    P.pallas_profile_enable(P.KERNEL_CLASSES)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = torch.cuda.Event(enable_timing=True)

@@ -38,13 +38,16 @@ __device__ __forceinline__ int kswz(int key, int c) {
   return D == 128 ? (c ^ (key & 15)) : (c ^ ((key >> 1) & 7));
 }
 
-template <int D>
-__global__ __launch_bounds__(512) void attn_prefill_kernel(AttnParams p, RowMap rm, AttnSched sch) {
-  constexpr int CH = D / 8;  // 16-byte chunks per K/V row
-  __shared__ __attribute__((aligned(16))) u32x4 Ks[KB * CH];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * (KB + VPAD)];
+template <int D, int G>
+__global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowMap rm, AttnSched sch) {
+  constexpr int CH = D / 8;                   // 16-byte chunks per K/V row
+  constexpr int ITEMS = (KB / 2) * CH;        // (key pair, chunk) staging items per tile
+  constexpr int VROW = KB + VPAD;
+  constexpr int nthreads = G * 64;
+  constexpr int MAXIT = (ITEMS + nthreads - 1) / nthreads;
+  __shared__ __attribute__((aligned(16))) u32x4 Ks[2][KB * CH];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VROW];
 
-  const int G = p.Hq / p.Hkv;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int g = lane >> 5, l32 = lane & 31;
   const int kh = blockIdx.y;
@@ -73,46 +76,68 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(AttnParams p, RowMap 
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int t = 0; t < D / 32; ++t) oacc[t] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;   // running max of raw scores; running sum
 
   const int kend = min(q0 + QB, len);
   const int ntiles = (kend + KB - 1) / KB;
-  const int nthreads = G * 64;
+  // Staging registers: each thread owns MAXIT (key pair, chunk) items.
+  u32x4 sk[MAXIT][2], sv[MAXIT][2];
 
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int k0 = kt * KB;
-    __syncthreads();
-    // Stage K (row-major, swizzled) and V (transposed) for keys k0..k0+63.
-    for (int it = threadIdx.x; it < (KB / 2) * CH; it += nthreads) {
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int r = 0; r < MAXIT; ++r) {
+      const int it = threadIdx.x + r * nthreads;
+      if (it >= ITEMS) break;
       const int kp = it % (KB / 2), ch = it / (KB / 2);
-      u32x4 kv[2], vv[2];
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const int key = 2 * kp + e;
-        const int pos = k0 + key;
-        kv[e] = u32x4{0, 0, 0, 0};
-        vv[e] = u32x4{0, 0, 0, 0};
+        const int pos = k0 + 2 * kp + e;
+        sk[r][e] = u32x4{0, 0, 0, 0};
+        sv[r][e] = u32x4{0, 0, 0, 0};
         if (pos < len) {
           const int pg = bt[pos / p.page];
           if (pg >= 0 && pg < p.num_pages) {
             const int64_t off = ((static_cast<int64_t>(pg) * p.page + pos % p.page) * p.Hkv + kh) * D + ch * 8;
-            kv[e] = *reinterpret_cast<const u32x4*>(p.k_plane + off);
-            vv[e] = *reinterpret_cast<const u32x4*>(p.v_plane + off);
+            sk[r][e] = *reinterpret_cast<const u32x4*>(p.k_plane + off);
+            sv[r][e] = *reinterpret_cast<const u32x4*>(p.v_plane + off);
           }
         }
-        Ks[key * CH + kswz<D>(key, ch)] = kv[e];
-      }
-      // Vt[dv][key]: pack keys (2kp, 2kp+1) for each of the 8 dv of this chunk
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t a = vv[0][e], b = vv[1][e];
-        const uint32_t lo = (a & 0xFFFFu) | (b << 16);
-        const uint32_t hi = (a >> 16) | (b & 0xFFFF0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * e) * (KB + VPAD) + 2 * kp]) = lo;
-        *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * e + 1) * (KB + VPAD) + 2 * kp]) = hi;
       }
     }
-    __syncthreads();
+  };
+  auto swrite = [&](int buf) {
+#pragma unroll
+    for (int r = 0; r < MAXIT; ++r) {
+      const int it = threadIdx.x + r * nthreads;
+      if (it >= ITEMS) break;
+      const int kp = it % (KB / 2), ch = it / (KB / 2);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int key = 2 * kp + e;
+        Ks[buf][key * CH + kswz<D>(key, ch)] = sk[r][e];
+      }
+      // Vt[dv][key]: keys (2kp, 2kp+1) packed per dv of this chunk
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t a = sv[r][0][e], b = sv[r][1][e];
+        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * VROW + 2 * kp]) = (a & 0xFFFFu) | (b << 16);
+        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * VROW + 2 * kp]) = (a >> 16) | (b & 0xFFFF0000u);
+      }
+    }
+  };
+
+  if (ntiles > 0) {
+    gload(0);
+    swrite(0);
+    if (ntiles > 1) gload(KB);
+  }
+  const float c = p.scale_log2;
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int buf = kt & 1;
+    const int k0 = kt * KB;
+    __syncthreads();  // tile kt resident; buffer buf^1 free
+    const u32x4* Kb = Ks[buf];
+    const uint16_t* Vb = Vt[buf];
 
     // S^T for keys k0 + [0,32) and k0 + [32,64)
     f32x16 st[2];
@@ -122,31 +147,35 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(AttnParams p, RowMap 
       const int key = t * 32 + l32;
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, Ks[key * CH + kswz<D>(key, kk * 2 + g)]);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, Kb[key * CH + kswz<D>(key, kk * 2 + g)]);
         st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], st[t], 0, 0, 0);
       }
+    }
+    // Masks only where the tile reaches the diagonal or the sequence end.
+    if (k0 + KB - 1 > q0 || k0 + KB > len) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + t * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          if (key > qpos || key >= len) st[t][r] = -INFINITY;
+        }
     }
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + t * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-        float v = st[t][r] * p.scale_log2;
-        if (key > qpos || key >= len) v = -INFINITY;
-        st[t][r] = v;
-        mx = fmaxf(mx, v);
-      }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[t][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+    const float mc = (m_new == -INFINITY) ? 0.f : m_new * c;
+    const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
     float rs = 0.f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(st[t][r] - m_use);
+        const float e = __builtin_amdgcn_exp2f(fmaf(st[t][r], c, -mc));
         st[t][r] = e;
         rs += e;
       }
@@ -157,21 +186,26 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(AttnParams p, RowMap 
     for (int t = 0; t < D / 32; ++t) oacc[t] *= alpha;
 
 #pragma unroll
-    for (int c = 0; c < KB / 16; ++c) {
-      const int t = c >> 1, base = (c & 1) * 8;
+    for (int cc = 0; cc < KB / 16; ++cc) {
+      const int t = cc >> 1, base = (cc & 1) * 8;
       u32x4 pk;
 #pragma unroll
       for (int e = 0; e < 4; ++e) pk[e] = pack_bf2(st[t][base + 2 * e], st[t][base + 2 * e + 1]);
       const bf16x8 pb = __builtin_bit_cast(bf16x8, pk);
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        const uint16_t* vrow = &Vt[(dt * 32 + l32) * (KB + VPAD) + c * 16 + g * 4];
+        const uint16_t* vrow = &Vb[(dt * 32 + l32) * VROW + cc * 16 + g * 4];
         const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
         const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 8);
         const u32x4 av = {lo.x, lo.y, hi.x, hi.y};
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pb,
                                                            oacc[dt], 0, 0, 0);
       }
+    }
+    // Stage tile kt+1 (loaded during this tile) and start loading kt+2.
+    if (kt + 1 < ntiles) {
+      swrite(buf ^ 1);
+      if (kt + 2 < ntiles) gload((kt + 2) * KB);
     }
   }
 
@@ -282,14 +316,30 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
   float o[kMaxG];
 #pragma unroll
   for (int g = 0; g < kMaxG; ++g) o[g] = 0.f;
-  for (int jj = kg; jj < jn; jj += NG) {
-    const int j = j0 + jj;
-    const int pg = bt[j / p.page];
-    if (pg < 0 || pg >= p.num_pages) continue;
-    const float v = bf2f(p.v_plane[((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D + dv]);
+  // Eight keys per round so eight V loads are in flight.
+  constexpr int U = 8;
+  for (int jb = kg; jb < jn; jb += NG * U) {
+    float v[U];
 #pragma unroll
-    for (int g = 0; g < kMaxG; ++g)
-      if (g < G) o[g] += sc[g][jj] * v;
+    for (int u = 0; u < U; ++u) {
+      const int jj = jb + u * NG;
+      v[u] = 0.f;
+      if (jj < jn) {
+        const int j = j0 + jj;
+        const int pg = bt[j / p.page];
+        if (pg >= 0 && pg < p.num_pages)
+          v[u] = bf2f(p.v_plane[((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D + dv]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int jj = jb + u * NG;
+      if (jj < jn) {
+#pragma unroll
+        for (int g = 0; g < kMaxG; ++g)
+          if (g < G) o[g] += sc[g][jj] * v[u];
+      }
+    }
   }
 #pragma unroll
   for (int g = 0; g < kMaxG; ++g)
@@ -345,12 +395,12 @@ hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipSt
   if (sch.total == 0) return hipSuccess;
   const int G = p.Hq / p.Hkv;
   dim3 grid(sch.total, p.Hkv);
-  if (p.d == 128)
-    attn_prefill_kernel<128><<<grid, G * 64, 0, s>>>(p, rm, sch);
-  else if (p.d == 64)
-    attn_prefill_kernel<64><<<grid, G * 64, 0, s>>>(p, rm, sch);
-  else
-    return hipErrorInvalidValue;
+#define PALLAS_ATTN_CASE(DD, GG) \
+  if (p.d == DD && G == GG) { attn_prefill_kernel<DD, GG><<<grid, GG * 64, 0, s>>>(p, rm, sch); return hipGetLastError(); }
+  PALLAS_ATTN_CASE(128, 1) PALLAS_ATTN_CASE(128, 2) PALLAS_ATTN_CASE(128, 4) PALLAS_ATTN_CASE(128, 8)
+  PALLAS_ATTN_CASE(64, 1) PALLAS_ATTN_CASE(64, 2) PALLAS_ATTN_CASE(64, 4) PALLAS_ATTN_CASE(64, 8)
+#undef PALLAS_ATTN_CASE
+  return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -231,8 +231,9 @@ int check_cfg(const pallas_model_config* c) {
     return fail(PALLAS_ERR_UNSUPPORTED, "model: page_size %d (supported: 16)", c->page_size);
   if (c->hidden % 64 != 0 || c->ffn % 16 != 0)
     return fail(PALLAS_ERR_UNSUPPORTED, "model: hidden must be a multiple of 64 and ffn of 16");
-  if (c->n_q_heads / c->n_kv_heads > 8)
-    return fail(PALLAS_ERR_UNSUPPORTED, "model: more than 8 query heads per KV head");
+  const int grp = c->n_q_heads / c->n_kv_heads;
+  if (grp != 1 && grp != 2 && grp != 4 && grp != 8)
+    return fail(PALLAS_ERR_UNSUPPORTED, "model: %d query heads per KV head (supported: 1, 2, 4, 8)", grp);
   return PALLAS_OK;
 }
 
@@ -247,15 +248,15 @@ int pallas_model_create(const pallas_model_config* cfg, const pallas_weights* w,
   if (int rc = check_cfg(cfg)) return rc;
   if (!w->embed || !w->final_norm || !w->lm_head || !w->layers)
     return fail(PALLAS_ERR_INVALID_ARG, "model: null global weight");
-  if (!aligned16(w->embed) || !aligned16(w->lm_head))
+  if (!aligned16(w->embed) || !aligned16(w->lm_head) || !aligned16(w->final_norm))
     return fail(PALLAS_ERR_INVALID_ARG, "model: weights must be 16-byte aligned");
   for (int l = 0; l < cfg->n_layers; ++l) {
     const pallas_layer_weights& L = w->layers[l];
     const void* need[] = {L.attn_norm, L.w_qkv, L.w_o, L.mlp_norm, L.w_gate_up, L.w_down};
     for (const void* p : need)
       if (!p || !aligned16(p)) return fail(PALLAS_ERR_INVALID_ARG, "model: layer %d weight null or unaligned", l);
-    if (cfg->qk_norm && (!L.q_norm || !L.k_norm))
-      return fail(PALLAS_ERR_INVALID_ARG, "model: layer %d lacks QK-norm gains", l);
+    if (cfg->qk_norm && (!L.q_norm || !L.k_norm || !aligned16(L.q_norm) || !aligned16(L.k_norm)))
+      return fail(PALLAS_ERR_INVALID_ARG, "model: layer %d QK-norm gains null or unaligned", l);
   }
   pallas_model* m = new pallas_model;
   m->cfg = *cfg;

@@ -5,8 +5,7 @@
 // (K after rotary; V copied bit for bit).  Q goes to a [rows][Hq][d]
 // buffer for the attention kernel.
 //
-// One wave per (row, head).  Lane i < d/2 holds the rotary pair (i, i+d/2),
-// so the norm is one wave sum and the rotation is lane-local.
+// One workgroup per row; each lane handles four rotary pairs of one head.
 #include "common.h"
 #include "kernels.h"
 
@@ -16,67 +15,102 @@ namespace {
 
 constexpr int kThreads = 256;
 
-__global__ __launch_bounds__(kThreads) void qkv_rope_kernel(QkvParams p, RowMap rm, int rows,
-                                                            int heads) {
-  const int wave_id = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  if (wave_id >= rows * heads) return;
-  const int lane = threadIdx.x & 63;
-  const int row = wave_id / heads;
-  const int hh = wave_id - row * heads + (p.kv_only ? p.Hq : 0);  // head in [0, Hq + 2 Hkv)
-  const int half = p.d >> 1;
-  const bool active = lane < half;
-  const int i = active ? lane : 0;
-
-  const int col0 = (p.kv_only ? hh - p.Hq : hh) * p.d;
-  const uint16_t* src = p.qkv + static_cast<int64_t>(row) * p.qkv_ld + col0;
-  const uint16_t b0 = src[i], b1 = src[i + half];
-
-  const bool is_q = hh < p.Hq;
-  const bool is_k = !is_q && hh < p.Hq + p.Hkv;
-  uint16_t o0 = b0, o1 = b1;
-  if (is_q || is_k) {
-    float x0 = bf2f(b0), x1 = bf2f(b1);
-    if (p.qk_norm) {
-      const float ss = wave_sum(active ? x0 * x0 + x1 * x1 : 0.f);
-      const float inv = rsqrtf(ss / p.d + p.eps);
-      const uint16_t* g = is_q ? p.q_gain : p.k_gain;
-      x0 = x0 * inv * bf2f(g[i]);
-      x1 = x1 * inv * bf2f(g[i + half]);
-    }
-    const float cs = p.rope[(static_cast<int64_t>(row) * half + i) * 2];
-    const float sn = p.rope[(static_cast<int64_t>(row) * half + i) * 2 + 1];
-    o0 = f2bf(x0 * cs - x1 * sn);
-    o1 = f2bf(x1 * cs + x0 * sn);
-  }
-  if (!active) return;
-  if (is_q) {
-    uint16_t* dst = p.q_out + (static_cast<int64_t>(row) * p.Hq + hh) * p.d;
-    dst[i] = o0;
-    dst[i + half] = o1;
-    return;
-  }
+// One workgroup per row.  A lane owns 4 rotary pairs: elements [4j, 4j+4)
+// of the head's first half and their partners [4j+d/2, 4j+d/2+4), loaded as
+// 8-byte vectors; d/8 lanes cover a head, so a workgroup works on
+// 256 / (d/8) heads at a time and the head norm is a sum over d/8 lanes.
+template <int D>
+__global__ __launch_bounds__(kThreads) void qkv_rope_kernel(QkvParams p, RowMap rm, int heads) {
+  constexpr int LPH = D / 8;            // lanes per head
+  constexpr int HPB = kThreads / LPH;   // heads per pass
+  constexpr int HALF = D / 2;
+  const int row = blockIdx.x;
+  const int j = threadIdx.x % LPH;      // pair group: pairs 4j .. 4j+3
+  const int hsub = threadIdx.x / LPH;
   const int s = row_seq(rm, row);
   const int pos = rm.base_pos[s] + (row - rm.cu[s]);
   const int pg = p.bt[static_cast<int64_t>(s) * p.max_pages + pos / p.page];
-  if (pg < 0 || pg >= p.num_pages) {
-    if (lane == 0 && p.err) atomicOr(p.err, static_cast<int32_t>(PALLAS_DEVERR_PAGE));
-    return;
+  const bool page_ok = pg >= 0 && pg < p.num_pages;
+  const int64_t slot = (static_cast<int64_t>(pg) * p.page + pos % p.page) * p.Hkv;
+  const f32x4* rope = reinterpret_cast<const f32x4*>(p.rope + (static_cast<int64_t>(row) * HALF + 4 * j) * 2);
+  const f32x4 cs01 = rope[0], cs23 = rope[1];   // (cos, sin) of pairs 4j .. 4j+3
+  const float cs[4] = {cs01.x, cs01.z, cs23.x, cs23.z};
+  const float sn[4] = {cs01.y, cs01.w, cs23.y, cs23.w};
+  const uint16_t* src_row = p.qkv + static_cast<int64_t>(row) * p.qkv_ld;
+  bool flagged = false;
+
+  for (int h0 = 0; h0 < heads; h0 += HPB) {
+    const int hl = h0 + hsub;                   // local head index
+    const bool active = hl < heads;
+    const int hh = hl + (p.kv_only ? p.Hq : 0); // head in [0, Hq + 2 Hkv)
+    const bool is_q = hh < p.Hq;
+    const bool is_k = !is_q && hh < p.Hq + p.Hkv;
+    u32x2 lo = {0, 0}, hi = {0, 0};
+    if (active) {
+      const uint16_t* src = src_row + static_cast<int64_t>(hl) * D;
+      lo = *reinterpret_cast<const u32x2*>(src + 4 * j);
+      hi = *reinterpret_cast<const u32x2*>(src + HALF + 4 * j);
+    }
+    float x0[4] = {bflo(lo.x), bfhi(lo.x), bflo(lo.y), bfhi(lo.y)};
+    float x1[4] = {bflo(hi.x), bfhi(hi.x), bflo(hi.y), bfhi(hi.y)};
+    u32x2 olo = lo, ohi = hi;
+    if (is_q || is_k) {
+      if (p.qk_norm) {
+        float ss = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ss += x0[e] * x0[e] + x1[e] * x1[e];
+#pragma unroll
+        for (int o = LPH / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
+        const float inv = rsqrtf(ss / D + p.eps);
+        const uint16_t* gsrc = is_q ? p.q_gain : p.k_gain;
+        const u32x2 g0 = *reinterpret_cast<const u32x2*>(gsrc + 4 * j);
+        const u32x2 g1 = *reinterpret_cast<const u32x2*>(gsrc + HALF + 4 * j);
+        const float ga[4] = {bflo(g0.x), bfhi(g0.x), bflo(g0.y), bfhi(g0.y)};
+        const float gb[4] = {bflo(g1.x), bfhi(g1.x), bflo(g1.y), bfhi(g1.y)};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x0[e] = x0[e] * inv * ga[e];
+          x1[e] = x1[e] * inv * gb[e];
+        }
+      }
+      float y0[4], y1[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        y0[e] = x0[e] * cs[e] - x1[e] * sn[e];
+        y1[e] = x1[e] * cs[e] + x0[e] * sn[e];
+      }
+      olo = u32x2{pack_bf2(y0[0], y0[1]), pack_bf2(y0[2], y0[3])};
+      ohi = u32x2{pack_bf2(y1[0], y1[1]), pack_bf2(y1[2], y1[3])};
+    }
+    if (!active) continue;
+    uint16_t* dst;
+    if (is_q) {
+      dst = p.q_out + (static_cast<int64_t>(row) * p.Hq + hh) * D;
+    } else {
+      if (!page_ok) {
+        flagged = true;
+        continue;
+      }
+      const int kh = is_k ? hh - p.Hq : hh - p.Hq - p.Hkv;
+      dst = (is_k ? p.k_plane : p.v_plane) + (slot + kh) * D;
+    }
+    *reinterpret_cast<u32x2*>(dst + 4 * j) = olo;
+    *reinterpret_cast<u32x2*>(dst + HALF + 4 * j) = ohi;
   }
-  const int kh = is_k ? hh - p.Hq : hh - p.Hq - p.Hkv;
-  uint16_t* plane = is_k ? p.k_plane : p.v_plane;
-  uint16_t* dst = plane + ((static_cast<int64_t>(pg) * p.page + pos % p.page) * p.Hkv + kh) * p.d;
-  dst[i] = o0;
-  dst[i + half] = o1;
+  if (flagged && j == 0 && p.err) atomicOr(p.err, static_cast<int32_t>(PALLAS_DEVERR_PAGE));
 }
 
 }  // namespace
 
 hipError_t launch_qkv_rope(const QkvParams& p, const RowMap& rm, int rows, hipStream_t s) {
   const int heads = p.kv_only ? 2 * p.Hkv : p.Hq + 2 * p.Hkv;
-  const int waves = rows * heads;
-  if (waves <= 0) return hipSuccess;
-  const int per_block = kThreads / 64;
-  qkv_rope_kernel<<<(waves + per_block - 1) / per_block, kThreads, 0, s>>>(p, rm, rows, heads);
+  if (rows <= 0) return hipSuccess;
+  if (p.d == 128)
+    qkv_rope_kernel<128><<<rows, kThreads, 0, s>>>(p, rm, heads);
+  else if (p.d == 64)
+    qkv_rope_kernel<64><<<rows, kThreads, 0, s>>>(p, rm, heads);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
