@@ -13,7 +13,7 @@
 // Softmax runs in fp32 in the log2 domain (scores pre-scaled by
 // log2(e)/sqrt(d)); P is rounded to bf16 for the PV product.
 //
-// Decode: split over keys (256 per workgroup, all query heads of one KV
+// Decode: split over keys (64 per workgroup, all query heads of one KV
 // head per workgroup), then a combine pass over the splits.
 #include <algorithm>
 
@@ -225,21 +225,26 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
 }
 
 constexpr int kDecThreads = 256;
-constexpr int kDecSplit = 256;  // keys per split (one key per thread in the score pass)
+constexpr int kDecSplit = 64;   // keys per split
 constexpr int kMaxG = 8;
 
-// Decode attention, split over keys: workgroup (seq, KV head, split) scores
-// its 256 keys for all G query heads of the KV head (each K row is read
+// Decode attention, split over keys: workgroup (split of 64 keys, KV head,
+// seq) scores its keys for all G query heads of the KV head (4 threads per
+// key, each over a quarter of the head dimension, so every K row is read
 // once), keeps the split's max, sum and unnormalised output per head in the
 // partial buffer; decode_combine merges the splits.
 template <int D>
 __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnParams p, RowMap rm,
                                                                         float* __restrict__ part,
                                                                         int max_splits) {
+  constexpr int TPK = kDecThreads / kDecSplit;  // threads per key (4)
+  constexpr int DPT = D / TPK;                  // dimensions per thread
+  constexpr int NG = kDecThreads / D;           // key groups in the PV pass
+  constexpr int KPG = kDecSplit / NG;           // keys per group
   __shared__ float qs[kMaxG][D];
   __shared__ float sc[kMaxG][kDecSplit];
-  __shared__ float red[kMaxG][kDecThreads / 64];
-  __shared__ float oacc[kDecThreads / D][kMaxG][D];
+  __shared__ float stat[kMaxG][2];
+  __shared__ float oacc[NG][kMaxG][D];
   const int G = p.Hq / p.Hkv;
   const int split = blockIdx.x, kh = blockIdx.y, s = blockIdx.z;
   const int n = rm.base_pos[s];
@@ -252,77 +257,77 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
     qs[i / D][i % D] = bf2f(p.q[(static_cast<int64_t>(row) * p.Hq + kh * G + i / D) * D + i % D]);
   __syncthreads();
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float sv[kMaxG];
+  // Scores: thread (key, quarter).
+  const int key = threadIdx.x / TPK, qt = threadIdx.x % TPK;
+  float acc[kMaxG];
 #pragma unroll
-  for (int g = 0; g < kMaxG; ++g) sv[g] = -INFINITY;
-  if (threadIdx.x < jn) {
-    const int j = j0 + threadIdx.x;
+  for (int g = 0; g < kMaxG; ++g) acc[g] = 0.f;
+  bool valid = false;
+  if (key < jn) {
+    const int j = j0 + key;
     const int pg = bt[j / p.page];
     if (pg >= 0 && pg < p.num_pages) {
-      const uint16_t* k = p.k_plane + ((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D;
-      float acc[kMaxG];
+      valid = true;
+      const uint16_t* k = p.k_plane + ((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D + qt * DPT;
+      u32x4 w[DPT / 8];
 #pragma unroll
-      for (int g = 0; g < kMaxG; ++g) acc[g] = 0.f;
-#pragma unroll 4
-      for (int c = 0; c < D / 8; ++c) {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(k + c * 8);
+      for (int c = 0; c < DPT / 8; ++c) w[c] = *reinterpret_cast<const u32x4*>(k + c * 8);
+#pragma unroll
+      for (int c = 0; c < DPT / 8; ++c) {
         float kf[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          kf[2 * e] = bflo(w[e]);
-          kf[2 * e + 1] = bfhi(w[e]);
+          kf[2 * e] = bflo(w[c][e]);
+          kf[2 * e + 1] = bfhi(w[c][e]);
         }
 #pragma unroll
         for (int g = 0; g < kMaxG; ++g) {
           if (g < G) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[g] += qs[g][c * 8 + e] * kf[e];
+            for (int e = 0; e < 8; ++e) acc[g] += qs[g][qt * DPT + c * 8 + e] * kf[e];
           }
         }
       }
-#pragma unroll
-      for (int g = 0; g < kMaxG; ++g) sv[g] = acc[g] * p.scale_log2;
     }
   }
-  // per-head max over the split
 #pragma unroll
   for (int g = 0; g < kMaxG; ++g) {
-    if (g >= G) break;
-    const float m = wave_max(sv[g]);
-    if (lane == 0) red[g][wave] = m;
+    acc[g] += __shfl_xor(acc[g], 1, kWave);
+    acc[g] += __shfl_xor(acc[g], 2, kWave);
   }
-  __syncthreads();
-  float mx[kMaxG];
+  if (qt == 0 && key < kDecSplit) {
 #pragma unroll
-  for (int g = 0; g < kMaxG; ++g) {
-    mx[g] = -INFINITY;
-    if (g < G)
-      for (int w = 0; w < kDecThreads / 64; ++w) mx[g] = fmaxf(mx[g], red[g][w]);
+    for (int g = 0; g < kMaxG; ++g)
+      if (g < G) sc[g][key] = valid ? acc[g] * p.scale_log2 : -INFINITY;
   }
   __syncthreads();
-#pragma unroll
-  for (int g = 0; g < kMaxG; ++g) {
-    if (g >= G) break;
-    const float e = (mx[g] == -INFINITY) ? 0.f : exp2f(sv[g] - mx[g]);
-    sc[g][threadIdx.x] = e;
-    const float t = wave_sum(e);
-    if (lane == 0) red[g][wave] = t;
+  // Per-head max and sum over the split: wave w owns heads w, w + 4.
+  {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    for (int g = wave; g < G; g += kDecThreads / 64) {
+      const float v = sc[g][lane];
+      const float m = wave_max(v);
+      const float e = (m == -INFINITY) ? 0.f : exp2f(v - m);
+      sc[g][lane] = e;
+      const float l = wave_sum(e);
+      if (lane == 0) {
+        stat[g][0] = m;
+        stat[g][1] = l;
+      }
+    }
   }
   __syncthreads();
-  // weighted sum of V: thread (key group kg, dim dv)
-  constexpr int NG = kDecThreads / D;
+  // Weighted sum of V: thread (dim dv, key group kg), eight V loads in flight.
   const int dv = threadIdx.x % D, kg = threadIdx.x / D;
   float o[kMaxG];
 #pragma unroll
   for (int g = 0; g < kMaxG; ++g) o[g] = 0.f;
-  // Eight keys per round so eight V loads are in flight.
-  constexpr int U = 8;
-  for (int jb = kg; jb < jn; jb += NG * U) {
-    float v[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int jj = jb + u * NG;
+  for (int jb = 0; jb < KPG; jb += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int jj = kg * KPG + jb + u;
       v[u] = 0.f;
       if (jj < jn) {
         const int j = j0 + jj;
@@ -332,13 +337,11 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
       }
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int jj = jb + u * NG;
-      if (jj < jn) {
+    for (int u = 0; u < 8; ++u) {
+      const int jj = kg * KPG + jb + u;
 #pragma unroll
-        for (int g = 0; g < kMaxG; ++g)
-          if (g < G) o[g] += sc[g][jj] * v[u];
-      }
+      for (int g = 0; g < kMaxG; ++g)
+        if (g < G) o[g] += sc[g][jj] * v[u];
     }
   }
 #pragma unroll
@@ -354,10 +357,8 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
     float* rec = part + ((static_cast<int64_t>(s) * p.Hq + kh * G + g) * max_splits + split) * (D + 2);
     rec[2 + e] = t;
     if (e == 0) {
-      float sum = 0.f;
-      for (int w = 0; w < kDecThreads / 64; ++w) sum += red[g][w];
-      rec[0] = mx[g];
-      rec[1] = sum;
+      rec[0] = stat[g][0];
+      rec[1] = stat[g][1];
     }
   }
 }

@@ -2,9 +2,10 @@
 // (activations [M][K], weights [N][K] as stored, [out][in]) and a float32
 // accumulator, with the epilogue fused into the store.
 //
-// Tiling: a 256 x 256 output tile per workgroup of 4 waves, each wave
-// 128 x 128 as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.  K advances 32 at
-// a time through a 4-deep LDS ring (4 x (16 KiB A + 16 KiB B)) filled by
+// Tiling: a 256 x 256 output tile per workgroup of 8 waves (two per SIMD,
+// so one wave's barrier and LDS waits overlap the other's MFMAs), each wave
+// 128 x 64 as 4 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 32 at
+// a time through a 5-deep LDS ring (5 x (16 KiB A + 16 KiB B)) filled by
 // buffer loads that write LDS directly (no register staging), issued three
 // K-steps ahead of the math so HBM latency hides behind three steps of
 // MFMA work; one barrier per step.  The buffer range check turns rows past
@@ -25,7 +26,7 @@ namespace {
 
 constexpr int BM = 256, BN = 256, BK = 32;
 constexpr int kStages = 5;               // LDS ring depth (5 x 32 KiB = all of LDS)
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;
 constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
 constexpr int kSlots = BM * kChunks;     // 16-byte slots per operand tile
 constexpr int kLoads = kSlots / kThreads;  // load instructions per thread per operand
@@ -97,20 +98,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)p.A, 0, p.a_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)p.B, 0, p.b_bytes, 0x00020000);
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   // LDS row of this lane's A fragment i and B fragment j
-  int arow[4], brow[4];
+  int arow[4], brow[2];
 #pragma unroll
   for (int i = 0; i < 4; ++i) arow[i] = wm * 128 + i * 32 + l32;
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    brow[j] = (EPI == kEpiSwiGLU ? (j >> 1) * 128 + wn * 64 + (j & 1) * 32 : wn * 128 + j * 32) + l32;
+  for (int j = 0; j < 2; ++j)
+    brow[j] = (EPI == kEpiSwiGLU ? j * 128 + wn * 32 : wn * 64 + j * 32) + l32;
 
   const int KT = (p.K + BK - 1) / BK;
   // Prologue: stages 0 .. kStages-2 in flight; then stage 0 resident.
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
 
   // Fragment registers: [k-half][block]; half 0 of step kt is read during
   // step kt-1, half 1 during the first half of step kt.
-  bf16x8 fa[2][4], fb[2][4];
+  bf16x8 fa[2][4], fb[2][2];
   auto read_frags = [&](int slot, int kk, bf16x8* a, bf16x8* b) {
     const u32x4* At = lds[slot][0];
     const u32x4* Bt = lds[slot][1];
@@ -135,13 +136,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) a[i] = __builtin_bit_cast(bf16x8, At[swz(arow[i], c)]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
+    for (int j = 0; j < 2; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
   };
   auto mfma_block = [&](const bf16x8* a, const bf16x8* b) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   };
   read_frags(0, 0, fa[0], fb[0]);
@@ -162,8 +163,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     read_frags(slot, 1, fa[1], fb[1]);
     mfma_block(fa[0], fb[0]);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // 2 MFMA
+    for (int q = 0; q < 6; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
     }
     if (kRefill)
@@ -176,8 +177,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     read_frags((kt + 1) % kStages, 0, fa[0], fb[0]);
     mfma_block(fa[1], fb[1]);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    for (int q = 0; q < 6; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
   };
@@ -196,17 +197,17 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
       if (EPI == kEpiSwiGLU) {
         uint16_t* C = static_cast<uint16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc;
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const int col = tn * (BN / 2) + wn * 64 + jj * 32 + l32;
+        for (int jj = 0; jj < 1; ++jj) {
+          const int col = tn * (BN / 2) + wn * 32 + l32;
           if (col < p.N) {
-            const float gt = acc[i][jj][r], up = acc[i][jj + 2][r];
+            const float gt = acc[i][0][r], up = acc[i][1][r];
             C[col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
           }
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int col = tn * BN + wn * 128 + j * 32 + l32;
+        for (int j = 0; j < 2; ++j) {
+          const int col = tn * BN + wn * 64 + j * 32 + l32;
           if (col >= p.N) continue;
           if (EPI == kEpiAddF32) {
             float* C = static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc;

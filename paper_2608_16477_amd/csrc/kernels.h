@@ -132,10 +132,9 @@ struct AttnParams {
 // positions <= its own (positions start at base_pos = 0).
 hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipStream_t s);
 // Decode attention: one row per sequence at position base_pos[s], keys
-// [0, base_pos[s]] through the table, split in runs of 256 keys.  `partial`
+// [0, base_pos[s]] through the table, split in runs of 64 keys.  `partial`
 // holds [n_seqs][Hq][max_splits][d + 2] floats; needs
-// base_pos[s] / 256 < max_splits and Hq / Hkv <= 8.
-constexpr int kDecodeSplitKeys = 256;
+// base_pos[s] / 64 < max_splits and Hq / Hkv <= 8.
 hipError_t launch_attention_decode(const AttnParams& p, const RowMap& rm, float* partial,
                                    int max_splits, hipStream_t s);
 

@@ -24,9 +24,9 @@ struct Workspace {
 };
 
 // Decode positions are below this bound; decode attention keeps one partial
-// record per 256-key split.
+// record per 64-key split.
 constexpr int kDecodeMaxPos = 16384;
-constexpr int kDecodeMaxSplits = kDecodeMaxPos / 256;
+constexpr int kDecodeMaxSplits = kDecodeMaxPos / 64;
 
 inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens, int64_t seqs) {
   Workspace w;
