@@ -63,8 +63,32 @@ class Shape:
                      float(cfg.rms_eps), float(cfg.rope_theta))
 
 
+_DTYPE = np.float64
+
+
 def f64(a) -> np.ndarray:
-    return np.asarray(a, dtype=np.float64)
+    """Cast to the working precision (float64 unless ``precision`` is active)."""
+    return np.asarray(a, dtype=_DTYPE)
+
+
+class precision:
+    """Context manager that evaluates the forward in another floating type
+    (float32 to measure how bf16 rounding decisions drift with depth when
+    the arithmetic is float32 rather than float64).  The default is
+    float64."""
+
+    def __init__(self, dtype):
+        self.dtype = dtype
+
+    def __enter__(self):
+        global _DTYPE
+        self.saved, _DTYPE = _DTYPE, self.dtype
+        return self
+
+    def __exit__(self, *exc):
+        global _DTYPE
+        _DTYPE = self.saved
+        return False
 
 
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
@@ -80,9 +104,9 @@ def rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
     d = x.shape[-1]
     half = d // 2
     inv_freq = theta ** (-(2.0 * np.arange(half, dtype=np.float64)) / d)
-    ang = f64(pos)[:, None] * inv_freq[None, :]
-    c = np.cos(ang)[:, None, :]
-    s = np.sin(ang)[:, None, :]
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
+    c = f64(np.cos(ang))[:, None, :]
+    s = f64(np.sin(ang))[:, None, :]
     x1, x2 = x[..., :half], x[..., half:]
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
@@ -103,7 +127,7 @@ def causal_attention(q: np.ndarray, q_pos: np.ndarray, k: np.ndarray,
     G = Hq // Hkv
     key_pos = np.arange(S)
     visible = key_pos[None, :] <= np.asarray(q_pos)[:, None]
-    out = np.empty((T, Hq, d), dtype=np.float64)
+    out = np.empty((T, Hq, d), dtype=np.result_type(q, v))
     scale = 1.0 / math.sqrt(d)
     for h in range(Hq):
         kh = h // G
@@ -161,7 +185,7 @@ def layer(r: np.ndarray, pos: np.ndarray, k_prev: Optional[np.ndarray],
 
 
 def embed(ids: Sequence[int], glob: Dict) -> np.ndarray:
-    return f64(glob["embed"])[np.asarray(ids, dtype=np.int64)]
+    return f64(np.asarray(glob["embed"])[np.asarray(ids, dtype=np.int64)])
 
 
 def logits(r_rows: np.ndarray, glob: Dict, shp: Shape, rnd: Rounder = bf16_round) -> np.ndarray:

@@ -19,6 +19,13 @@ def bf16_round(x) -> np.ndarray:
     return np.rint(x / ulp) * ulp
 
 
+def bf16_round_as(x) -> np.ndarray:
+    """bf16 rounding that keeps the input's floating type (for forwards
+    evaluated in float32)."""
+    x = np.asarray(x)
+    return bf16_round(x.astype(np.float64)).astype(x.dtype)
+
+
 def no_round(x) -> np.ndarray:
     """Identity rounding: the same forward in plain float64."""
     return np.asarray(x, dtype=np.float64)

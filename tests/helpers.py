@@ -76,3 +76,27 @@ def rel_err(got: np.ndarray, ref: np.ndarray) -> float:
 
 
 TOL = 1e-2   # max|gpu - ref| <= TOL * max|ref| per (layer, K|V) tensor and per logits row
+
+
+class LazyOracleLayers:
+    """Per-layer float64 numpy weights, converted from device tensors on
+    access and kept only for the most recent layer (full-size models do not
+    fit in host memory at float64)."""
+
+    def __init__(self, layers):
+        self.layers = layers
+        self._cache = (None, None)
+
+    def __len__(self):
+        return len(self.layers)
+
+    def __getitem__(self, l):
+        if self._cache[0] != l:
+            self._cache = (l, {k: to_np64(v) for k, v in self.layers[l].items()})
+        return self._cache[1]
+
+
+def oracle_globals(glob, need_embed_rows=None):
+    """Float64 globals; the embedding is gathered to the rows needed."""
+    g = {k: to_np64(v) for k, v in glob.items() if k not in ("embed", "lm_head")}
+    return g
