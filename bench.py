@@ -35,6 +35,29 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+
+# Memory-side traffic of one gate|up GEMM launch at the large workload, from
+# two rocprofv3 --pmc passes over `bench.py --steps 1 --warmup 0
+# --no-cpu-baseline` (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch, averaged
+# over the 63 launches at M = 3000), each scaled by what the same counter
+# reads for a 1 GiB device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid
+# only for the GEMM source it was measured on: a different csrc/gemm.hip
+# reports null.
+GEMM_TRAFFIC = {
+    "gemm_source_sha256_16": "055fa846b0f66c15",
+    "fetch_kib": 2.833e6, "fetch_scale": 2.0,
+    "write_kib": 1.5e5, "write_scale": 1.0,
+}
+
+
+def gemm_traffic_bytes():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2608_16477_amd", "csrc", "gemm.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    t = GEMM_TRAFFIC
+    if sha != t["gemm_source_sha256_16"]:
+        return None
+    return (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
 METRIC = "prefix-prefill tokens/s + % bf16 MFMA peak; KV pack/assemble GB/s + % HBM peak"
 
 
@@ -293,7 +316,9 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": gemm_traffic_bytes(),
+            "algorithmic_bytes": 2.0 * (prefix_tokens * cfg.hidden + 2 * cfg.ffn * cfg.hidden
+                                        + prefix_tokens * cfg.ffn),
         },
         "cpu_baseline": None,
     }

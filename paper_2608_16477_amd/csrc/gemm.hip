@@ -4,12 +4,15 @@
 //
 // Tiling: a 256 x 256 output tile per workgroup of 8 waves (two per SIMD,
 // so one wave's barrier and LDS waits overlap the other's MFMAs), each wave
-// 128 x 64 as 4 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 32 at
-// a time through a 5-deep LDS ring (5 x (16 KiB A + 16 KiB B)) filled by
-// buffer loads that write LDS directly (no register staging), issued three
-// K-steps ahead of the math so HBM latency hides behind three steps of
-// MFMA work; one barrier per step.  The buffer range check turns rows past
-// M/N and columns past K into zeros.
+// 128 x 64 as 4 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at
+// a time through a double-buffered LDS stage (2 x (32 KiB A + 32 KiB B))
+// filled by buffer loads that write LDS directly (no register staging),
+// issued one K-step ahead; one barrier per step.  64-element K-steps make
+// every operand row segment a whole 128-byte line, so each L1 miss request
+// carries 128 bytes: the kernel is bound by how many misses a CU keeps in
+// flight against L2 latency, and full-line requests double the bytes per
+// request.  The buffer range check turns rows past M/N and columns past K
+// into zeros.
 //
 // Workgroups are dispatched round-robin over the 8 XCDs; the tile index is
 // remapped so each XCD owns a contiguous run of tiles, M-tile fastest, so
@@ -24,8 +27,9 @@ namespace pallas {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32;
-constexpr int kStages = 5;               // LDS ring depth (5 x 32 KiB = all of LDS)
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int kStages = 2;               // LDS ring depth (2 x 64 KiB)
+constexpr int KK = BK / 16;              // MFMA K-substeps per K-step
 constexpr int kThreads = 512;
 constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
 constexpr int kSlots = BM * kChunks;     // 16-byte slots per operand tile
@@ -34,10 +38,10 @@ constexpr int kXcds = 8;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// 64-byte rows: four rows span the 64 banks; XOR the chunk with (row / 4)
-// mod 4 so 16 consecutive rows read at one logical chunk hit 16 distinct
+// 128-byte rows: two rows span the 64 banks; XOR the chunk with (row / 2)
+// mod 8 so 16 consecutive rows read at one logical chunk hit 16 distinct
 // 4-bank groups.
-__device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 2) & 3)); }
+__device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 7)); }
 
 __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
                                               const int* row_off_valid, const int* chunk, int k0,
@@ -79,7 +83,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   for (int i = 0; i < kLoads; ++i) {
     const int s = (wave * kLoads + i) * 64 + lane;
     const int row = s / kChunks;
-    chunk[i] = (s % kChunks) ^ ((row >> 2) & 3);
+    chunk[i] = (s % kChunks) ^ ((row >> 1) & 7);
     const int gm = m0 + row;
     a_off[i] = gm < p.M ? gm * p.lda * 2 : -1;
     int gn;
@@ -147,10 +151,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   };
   read_frags(0, 0, fa[0], fb[0]);
 
-  // One K-step: refill the slot of step kt-1 (kRefill), MFMAs on half 0
-  // while half 1 is read, wait for stage kt+1 and barrier, MFMAs on half 1
-  // while half 0 of step kt+1 is read.  The steady loop has no branches so
-  // the LDS reads interleave with the MFMAs.
+  // One K-step: refill the slot of step kt-1 (kRefill); MFMAs on substep kk
+  // while substep kk+1 is read; before the last substep, wait for stage
+  // kt+1 and barrier; the last substep's MFMAs then overlap the reads of
+  // step kt+1's first substep.  The steady loop has no branches so the LDS
+  // reads interleave with the MFMAs.
   auto step = [&](int kt, auto refill_tag) {
     constexpr bool kRefill = decltype(refill_tag)::value;
     const int slot = kt % kStages;
@@ -160,12 +165,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
       load_tile_lds(ra, p.a_bytes, a_off, chunk, nk * BK, p.K, lds[ns][0], wave, lane);
       load_tile_lds(rb, p.b_bytes, b_off, chunk, nk * BK, p.K, lds[ns][1], wave, lane);
     }
-    read_frags(slot, 1, fa[1], fb[1]);
-    mfma_block(fa[0], fb[0]);
 #pragma unroll
-    for (int q = 0; q < 6; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+    for (int kk = 0; kk < KK - 1; ++kk) {
+      read_frags(slot, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
+      mfma_block(fa[kk & 1], fb[kk & 1]);
+#pragma unroll
+      for (int q = 0; q < 6; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+      }
     }
     if (kRefill)
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads * (kStages - 2)) : "memory");
@@ -174,8 +182,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     __builtin_amdgcn_s_barrier();
     // Step kt+1 is resident; its slot index is valid even past the end
     // (the fragments are then unused).
-    read_frags((kt + 1) % kStages, 0, fa[0], fb[0]);
-    mfma_block(fa[1], fb[1]);
+    read_frags((kt + 1) % kStages, 0, fa[KK & 1], fb[KK & 1]);
+    mfma_block(fa[(KK - 1) & 1], fb[(KK - 1) & 1]);
 #pragma unroll
     for (int q = 0; q < 6; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
