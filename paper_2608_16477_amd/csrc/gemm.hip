@@ -33,8 +33,13 @@ constexpr int KK = BK / 16;              // MFMA K-substeps per K-step
 constexpr int kThreads = 512;
 constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
 constexpr int kSlots = BM * kChunks;     // 16-byte slots per operand tile
-constexpr int kLoads = kSlots / kThreads;  // load instructions per thread per operand
+// Only waves 0-3 (one per SIMD) issue the operand loads: a wave blocked
+// on a full L1 miss queue cannot issue MFMAs, and this keeps waves 4-7
+// issuing MFMAs on every SIMD.
+constexpr int kLoaderWaves = 4;
+constexpr int kLoads = kSlots / (kLoaderWaves * 64);  // load instructions per loader thread per operand
 constexpr int kXcds = 8;
+constexpr int kGroupM = 6;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -46,8 +51,9 @@ __device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^
 __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
                                               const int* row_off_valid, const int* chunk, int k0,
                                               int K, u32x4* lds_tile, int wave, int lane) {
-  // kLoads instructions per wave; instruction i fills slots
+  // kLoads instructions per loader wave; instruction i fills slots
   // [(wave*kLoads+i)*64, +64).
+  if (wave >= kLoaderWaves) return;
 #pragma unroll
   for (int i = 0; i < kLoads; ++i) {
     const int base = (wave * kLoads + i) * 64;
@@ -69,7 +75,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   if (loc >= p.tiles_per_xcd) return;
   const int t = (bid % kXcds) * p.tiles_per_xcd + loc;
   if (t >= p.total_tiles) return;
-  const int tm = t % p.tiles_m, tn = t / p.tiles_m;
+  // Grouped order: runs of group_m M-tiles, M fastest, so the ~32
+  // workgroups an XCD runs at once cover about group_m x (32 / group_m)
+  // tiles and share both operand panels in its L2.
+  const int per_group = p.group_m * p.tiles_n;
+  const int first_m = (t / per_group) * p.group_m;
+  const int gsz = min(p.tiles_m - first_m, p.group_m);
+  const int tm = first_m + (t % per_group) % gsz;
+  const int tn = (t % per_group) / gsz;
   const int m0 = tm * BM;
 
   const int lane = threadIdx.x & 63;
@@ -256,6 +269,7 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   p.tiles_n = epi == kEpiSwiGLU ? (N + BN / 2 - 1) / (BN / 2) : (N + BN - 1) / BN;
   p.total_tiles = p.tiles_m * p.tiles_n;
   p.tiles_per_xcd = (p.total_tiles + kXcds - 1) / kXcds;
+  p.group_m = std::min(p.tiles_m, kGroupM);
   p.a_bytes = static_cast<uint32_t>(int64_t(M) * lda * 2);
   const int64_t brows = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
   p.b_bytes = static_cast<uint32_t>(brows * ldb * 2);

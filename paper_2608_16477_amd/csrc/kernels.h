@@ -53,7 +53,7 @@ struct GemmParams {
   void* C;
   int M, N, K;
   int lda, ldb, ldc;
-  int tiles_m, tiles_n, total_tiles, tiles_per_xcd;
+  int tiles_m, tiles_n, total_tiles, tiles_per_xcd, group_m;
   uint32_t a_bytes, b_bytes;
 };
 
