@@ -44,8 +44,8 @@ PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 # only for the GEMM source it was measured on: a different csrc/gemm.hip
 # reports null.
 GEMM_TRAFFIC = {
-    "gemm_source_sha256_16": "055fa846b0f66c15",
-    "fetch_kib": 2.833e6, "fetch_scale": 2.0,
+    "gemm_source_sha256_16": "463886a325c4457c",
+    "fetch_kib": 2.387e6, "fetch_scale": 2.0,
     "write_kib": 1.5e5, "write_scale": 1.0,
 }
 
