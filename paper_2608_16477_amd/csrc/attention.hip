@@ -371,14 +371,38 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnParams p, Ro
   const int n = rm.base_pos[s];
   const int nsplit = n / kDecSplit + 1;
   const float* base = part + (static_cast<int64_t>(s) * p.Hq + h) * max_splits * (D + 2);
-  float m = -INFINITY;
-  for (int k = 0; k < nsplit; ++k) m = fmaxf(m, base[k * (D + 2)]);
-  float l = 0.f, o = 0.f;
-  for (int k = 0; k < nsplit; ++k) {
-    const float* rec = base + k * (D + 2);
-    const float w = (rec[0] == -INFINITY) ? 0.f : exp2f(rec[0] - m);
-    l += w * rec[1];
-    o += w * rec[2 + threadIdx.x];
+  // Online merge, eight split records per round so their loads overlap.
+  constexpr int U = 8;
+  float m = -INFINITY, l = 0.f, o = 0.f;
+  for (int k0 = 0; k0 < nsplit; k0 += U) {
+    float mk[U], lk[U], ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = k0 + u;
+      mk[u] = -INFINITY;
+      lk[u] = 0.f;
+      ok[u] = 0.f;
+      if (k < nsplit) {
+        const float* rec = base + static_cast<int64_t>(k) * (D + 2);
+        mk[u] = rec[0];
+        lk[u] = rec[1];
+        ok[u] = rec[2 + threadIdx.x];
+      }
+    }
+    float mg = m;
+#pragma unroll
+    for (int u = 0; u < U; ++u) mg = fmaxf(mg, mk[u]);
+    if (mg == -INFINITY) continue;
+    const float sc = exp2f(m - mg);   // m = -inf -> 0
+    l *= sc;
+    o *= sc;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float w = exp2f(mk[u] - mg);
+      l += w * lk[u];
+      o += w * ok[u];
+    }
+    m = mg;
   }
   p.o[(static_cast<int64_t>(rm.cu[s]) * p.Hq + h) * D + threadIdx.x] = f2bf(l > 0.f ? o / l : 0.f);
 }
