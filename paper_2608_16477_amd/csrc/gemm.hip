@@ -53,7 +53,6 @@ __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint3
                                               int K, u32x4* lds_tile, int wave, int lane) {
   // kLoads instructions per loader wave; instruction i fills slots
   // [(wave*kLoads+i)*64, +64).
-  if (wave >= kLoaderWaves) return;
 #pragma unroll
   for (int i = 0; i < kLoads; ++i) {
     const int base = (wave * kLoads + i) * 64;
@@ -134,7 +133,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   // Prologue: stages 0 .. kStages-2 in flight; then stage 0 resident.
 #pragma unroll
   for (int st = 0; st < kStages - 1; ++st) {
-    if (st < KT) {
+    if (st < KT && wave < kLoaderWaves) {
       load_tile_lds(ra, p.a_bytes, a_off, chunk, st * BK, p.K, lds[st][0], wave, lane);
       load_tile_lds(rb, p.b_bytes, b_off, chunk, st * BK, p.K, lds[st][1], wave, lane);
     }
@@ -169,10 +168,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   // kt+1 and barrier; the last substep's MFMAs then overlap the reads of
   // step kt+1's first substep.  The steady loop has no branches so the LDS
   // reads interleave with the MFMAs.
-  auto step = [&](int kt, auto refill_tag) {
+  auto step = [&](int kt, auto refill_tag, auto loader_tag) {
     constexpr bool kRefill = decltype(refill_tag)::value;
+    constexpr bool kLoader = decltype(loader_tag)::value;
     const int slot = kt % kStages;
-    if (kRefill) {
+    if (kRefill && kLoader) {
       const int nk = kt + kStages - 1;
       const int ns = nk % kStages;
       load_tile_lds(ra, p.a_bytes, a_off, chunk, nk * BK, p.K, lds[ns][0], wave, lane);
@@ -182,10 +182,22 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     for (int kk = 0; kk < KK - 1; ++kk) {
       read_frags(slot, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
       mfma_block(fa[kk & 1], fb[kk & 1]);
+      if (kRefill && kLoader && kk == 0) {
+        // all refill loads ride between this substep's MFMAs
 #pragma unroll
-      for (int q = 0; q < 6; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+        for (int q = 0; q < 6; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // 2 global loads
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 6; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+        }
       }
     }
     if (kRefill)
@@ -203,9 +215,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
   };
-  int kt = 0;
-  for (; kt + kStages - 1 < KT; ++kt) step(kt, std::true_type{});
-  for (; kt < KT; ++kt) step(kt, std::false_type{});
+  // The K-loop is specialised per role so the loader waves' loads sit in
+  // the same scheduling region as their MFMAs.
+  auto main_loop = [&](auto loader_tag) {
+    int kt = 0;
+    for (; kt + kStages - 1 < KT; ++kt) step(kt, std::true_type{}, loader_tag);
+    for (; kt < KT; ++kt) step(kt, std::false_type{}, loader_tag);
+  };
+  if (wave < kLoaderWaves) main_loop(std::true_type{});
+  else main_loop(std::false_type{});
 
   // Epilogue.  Accumulator register r of block (i, j) holds
   // row wm*128 + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.
