@@ -88,7 +88,7 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
     for (int r = 0; r < MAXIT; ++r) {
       const int it = threadIdx.x + r * nthreads;
       if (it >= ITEMS) break;
-      const int kp = it % (KB / 2), ch = it / (KB / 2);
+      const int ch = it % CH, kp = it / CH;  // chunk fastest: lanes read whole head rows
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const int pos = k0 + 2 * kp + e;
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
     for (int r = 0; r < MAXIT; ++r) {
       const int it = threadIdx.x + r * nthreads;
       if (it >= ITEMS) break;
-      const int kp = it % (KB / 2), ch = it / (KB / 2);
+      const int ch = it % CH, kp = it / CH;  // chunk fastest: lanes read whole head rows
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const int key = 2 * kp + e;
