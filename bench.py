@@ -40,12 +40,13 @@ PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 # two rocprofv3 --pmc passes over `bench.py --steps 1 --warmup 0
 # --no-cpu-baseline` (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch, averaged
 # over the 63 launches at M = 3000), each scaled by what the same counter
-# reads for a 1 GiB device copy (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid
+# reads for a 1 GiB device copy (`bench.py --copy-calibration`: FETCH_SIZE
+# x 2.0, WRITE_SIZE x 1.0).  Valid
 # only for the GEMM source it was measured on: a different csrc/gemm.hip
 # reports null.
 GEMM_TRAFFIC = {
-    "gemm_source_sha256_16": "463886a325c4457c",
-    "fetch_kib": 2.387e6, "fetch_scale": 2.0,
+    "gemm_source_sha256_16": "a52580d27d4d79b9",
+    "fetch_kib": 2.082e6, "fetch_scale": 2.0,
     "write_kib": 1.5e5, "write_scale": 1.0,
 }
 
@@ -70,7 +71,22 @@ def parse():
                     choices=["tiny", "mid", "large", "large-aligned", "concurrent"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 1 GiB device-to-device copy and exit (the reference "
+                         "point for scaling FETCH_SIZE / WRITE_SIZE counter readings)")
     return ap.parse_args()
+
+
+def copy_calibration():
+    """One plain copy of known size: 2^28 int32 (1 GiB read, 1 GiB written)."""
+    import torch
+    n = (1 << 30) // 4
+    a = torch.ones(n, dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    print(f"[bench] copied {n * 4} bytes", file=sys.stderr, flush=True)
 
 
 def load_library():
@@ -209,6 +225,9 @@ def main():
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the reconstruction path runs on one GPU with no collectives).", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
     from workloads import workload
 
