@@ -46,6 +46,7 @@ extern "C" {
 
 #define PALLAS_ABI_VERSION 1
 #define PALLAS_MAX_SEQS 64 /* sequences per prefill or decode call */
+#define PALLAS_MAX_PREFILL_LEN 32768 /* tokens per sequence in one prefill call */
 
 typedef enum {
   PALLAS_OK = 0,
@@ -168,7 +169,8 @@ size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t 
  *   pool[l][0|1][bt_i[t / page]][t % page]
  * with bt_i = d_block_tables + i * max_pages (int32, device).  Nothing else
  * is written to the pool; no logits are produced.  num_seqs in
- * [1, PALLAS_MAX_SEQS]; p_i >= 1; sum p_i <= the workspace's max_tokens.
+ * [1, PALLAS_MAX_SEQS]; 1 <= p_i <= PALLAS_MAX_PREFILL_LEN (UNSUPPORTED
+ * beyond); sum p_i <= the workspace's max_tokens.
  * Table entries outside [0, num_pages) are skipped and raise
  * PALLAS_DEVERR_PAGE in *d_err (nullable, device, caller clears it). */
 int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,

@@ -5,13 +5,15 @@
 // pool once for all G query heads.  The score tile is computed transposed,
 // S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: a lane then owns one query and
 // 16 of its keys per 32-key block, so the online-softmax max and sum are
-// register reductions plus one cross-half shuffle, and the rescale of the
+// register reductions plus one cross-half lane swap, and the rescale of the
 // output accumulator is lane-uniform.  O^T = V^T P^T reuses the score
 // registers as the B operand; the key order inside each 16-key MFMA step is
 // permuted identically on both operands (a sum is order-free), which lets V
 // be read from a transposed LDS tile with two 8-byte reads per step.
-// Softmax runs in fp32 in the log2 domain (scores pre-scaled by
-// log2(e)/sqrt(d)); P is rounded to bf16 for the PV product.
+// Softmax runs in fp32 in the log2 domain (scores scaled by log2(e)/sqrt(d))
+// against a reference max that is raised lazily; P is rounded to bf16 for
+// the PV product.  The scores of tile j+1 are computed while tile j goes
+// through softmax and PV, so MFMA and VALU work of one wave overlap.
 //
 // Decode: split over keys (64 per workgroup, all query heads of one KV
 // head per workgroup), then a combine pass over the splits.
@@ -27,15 +29,24 @@ namespace {
 constexpr int QB = 32;  // queries per workgroup
 constexpr int KB = 64;  // keys per tile
 constexpr int VPAD = 4; // Vt row padding (elements): 136-byte rows spread banks
+constexpr int kPage = 16;     // tokens per cache page (the only page size the library accepts)
+constexpr int KSTR = KB + 1;  // K tile chunk stride, in 16-byte slots
+constexpr float kLazyLog2 = 8.f;  // lazy-rescale headroom, log2 units
 
 struct AttnSched {
   int32_t total;
   int32_t prefix[kMaxSeqs + 1];  // query blocks before sequence s
 };
 
-template <int D>
-__device__ __forceinline__ int kswz(int key, int c) {
-  return D == 128 ? (c ^ (key & 15)) : (c ^ ((key >> 1) & 7));
+// Full max / sum over the two 32-lane halves of a wave (the two key halves
+// of one query in the S^T layout).
+__device__ __forceinline__ float xhalf_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 template <int D, int G>
@@ -45,10 +56,14 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
   constexpr int VROW = KB + VPAD;
   constexpr int nthreads = G * 64;
   constexpr int MAXIT = (ITEMS + nthreads - 1) / nthreads;
-  __shared__ __attribute__((aligned(16))) u32x4 Ks[2][KB * CH];
+  // K tile as [chunk][key] with a chunk stride of KB + 1 slots: the score
+  // MFMA reads 32 consecutive keys of one chunk, and the staging writes of
+  // 16 chunks of one key pair land in distinct banks.
+  __shared__ __attribute__((aligned(16))) u32x4 Ks[2][CH * KSTR];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VROW];
+  __shared__ int32_t bts[kMaxPrefillLen / kPage];   // the sequence's block-table entries
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int g = lane >> 5, l32 = lane & 31;
   const int kh = blockIdx.y;
   const int h = kh * G + wave;
@@ -73,103 +88,118 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
     }
   }
 
-  f32x16 oacc[D / 32];
-#pragma unroll
-  for (int t = 0; t < D / 32; ++t) oacc[t] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;   // running max of raw scores; running sum
-
   const int kend = min(q0 + QB, len);
   const int ntiles = (kend + KB - 1) / KB;
-  // Staging registers: each thread owns MAXIT (key pair, chunk) items.
-  u32x4 sk[MAXIT][2], sv[MAXIT][2];
+  {
+    // This sequence's block-table entries for keys [0, kend), read once.
+    const int npages = (kend + kPage - 1) / kPage;
+    for (int i = threadIdx.x; i < npages; i += nthreads) bts[i] = bt[i];
+    __syncthreads();
+  }
 
-  auto gload = [&](int k0) {
+  // Element offsets of key `pos` (and of key pos + 1, same page: pairs start
+  // at even positions and pages hold 16) in a K/V plane, at this KV head.
+  // Keys at or past kend are masked for every query of the block; they read
+  // key kend - 1 instead (its table entry is staged, and a finite V row
+  // times probability zero adds nothing).  A table entry outside the pool
+  // reads page 0 (the K/V store reports such entries).
+  const int64_t row_stride = static_cast<int64_t>(p.Hkv) * D;
+  const uint16_t* kbase = p.k_plane + kh * D;
+  const uint16_t* vbase = p.v_plane + kh * D;
+  auto pair_off = [&](int pos, int64_t& off0, int64_t& off1) {
+    const int pc = min(pos, kend - 1);
+    int pg = bts[pc >> 4];
+    pg = (pg >= 0 && pg < p.num_pages) ? pg : 0;
+    off0 = (static_cast<int64_t>(pg) * kPage + (pc & (kPage - 1))) * row_stride;
+    off1 = off0 + (pos + 1 < kend ? row_stride : 0);
+  };
+  // Staging registers: each thread owns MAXIT (key pair, chunk) items.
+  u32x4 skr[MAXIT][2], svr[MAXIT][2];
+  auto gload = [&](u32x4 (&dst)[MAXIT][2], const uint16_t* base, int k0) {
 #pragma unroll
     for (int r = 0; r < MAXIT; ++r) {
       const int it = threadIdx.x + r * nthreads;
-      if (it >= ITEMS) break;
+      if (ITEMS % nthreads != 0 && it >= ITEMS) break;
       const int ch = it % CH, kp = it / CH;  // chunk fastest: lanes read whole head rows
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int pos = k0 + 2 * kp + e;
-        sk[r][e] = u32x4{0, 0, 0, 0};
-        sv[r][e] = u32x4{0, 0, 0, 0};
-        if (pos < len) {
-          const int pg = bt[pos / p.page];
-          if (pg >= 0 && pg < p.num_pages) {
-            const int64_t off = ((static_cast<int64_t>(pg) * p.page + pos % p.page) * p.Hkv + kh) * D + ch * 8;
-            sk[r][e] = *reinterpret_cast<const u32x4*>(p.k_plane + off);
-            sv[r][e] = *reinterpret_cast<const u32x4*>(p.v_plane + off);
-          }
-        }
-      }
+      int64_t o0, o1;
+      pair_off(k0 + 2 * kp, o0, o1);
+      dst[r][0] = *reinterpret_cast<const u32x4*>(base + o0 + ch * 8);
+      dst[r][1] = *reinterpret_cast<const u32x4*>(base + o1 + ch * 8);
     }
   };
-  auto swrite = [&](int buf) {
+  auto swriteK = [&](int buf) {
 #pragma unroll
     for (int r = 0; r < MAXIT; ++r) {
       const int it = threadIdx.x + r * nthreads;
-      if (it >= ITEMS) break;
-      const int ch = it % CH, kp = it / CH;  // chunk fastest: lanes read whole head rows
+      if (ITEMS % nthreads != 0 && it >= ITEMS) break;
+      const int ch = it % CH, kp = it / CH;
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int key = 2 * kp + e;
-        Ks[buf][key * CH + kswz<D>(key, ch)] = sk[r][e];
-      }
+      for (int e = 0; e < 2; ++e) Ks[buf][ch * KSTR + 2 * kp + e] = skr[r][e];
+    }
+  };
+  auto swriteV = [&](int buf) {
+#pragma unroll
+    for (int r = 0; r < MAXIT; ++r) {
+      const int it = threadIdx.x + r * nthreads;
+      if (ITEMS % nthreads != 0 && it >= ITEMS) break;
+      const int ch = it % CH, kp = it / CH;
       // Vt[dv][key]: keys (2kp, 2kp+1) packed per dv of this chunk
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint32_t a = sv[r][0][e], b = sv[r][1][e];
-        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * VROW + 2 * kp]) = (a & 0xFFFFu) | (b << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * VROW + 2 * kp]) = (a >> 16) | (b & 0xFFFF0000u);
+        const uint32_t a = svr[r][0][e], b = svr[r][1][e];
+        const int key = (2 * kp) ^ (8 * ((ch * 8) >> 5));   // 8-key swizzle by dv / 32
+        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * VROW + key]) = __builtin_amdgcn_perm(b, a, 0x05040100u);
+        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * VROW + key]) = __builtin_amdgcn_perm(b, a, 0x07060302u);
       }
     }
   };
+  auto barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
-  if (ntiles > 0) {
-    gload(0);
-    swrite(0);
-    if (ntiles > 1) gload(KB);
-  }
-  const float c = p.scale_log2;
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int buf = kt & 1;
-    const int k0 = kt * KB;
-    __syncthreads();  // tile kt resident; buffer buf^1 free
-    const u32x4* Kb = Ks[buf];
-    const uint16_t* Vb = Vt[buf];
-
-    // S^T for keys k0 + [0,32) and k0 + [32,64)
-    f32x16 st[2];
+  // S^T = K Q^T for one 64-key tile: keys t*32 + [0,32) in st[t].
+  auto scores = [&](int buf, f32x16 (&st)[2]) {
+    const u32x4* Kb = Ks[buf] + g * KSTR + l32;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      st[t] = f32x16{};
-      const int key = t * 32 + l32;
+    for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, Kb[key * CH + kswz<D>(key, kk * 2 + g)]);
-        st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], st[t], 0, 0, 0);
+      for (int t = 0; t < 2; ++t) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, Kb[kk * 2 * KSTR + t * 32]);
+        st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], kk == 0 ? f32x16{} : st[t], 0, 0, 0);
       }
-    }
-    // Masks only where the tile reaches the diagonal or the sequence end.
-    if (k0 + KB - 1 > q0 || k0 + KB > len) {
+    // Keep eight K-fragment reads in flight ahead of the MFMAs.
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+    for (int i = 0; i < 8; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + t * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-          if (key > qpos || key >= len) st[t][r] = -INFINITY;
-        }
+    for (int i = 0; i < D / 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i + 8 < D / 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
     }
+  };
+
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int t = 0; t < D / 32; ++t) oacc[t] = f32x16{};
+  // Probabilities are exp2((s - m_ref) c).  m_ref is raised only when a
+  // score exceeds it by more than kLazyLog2 / c, so probabilities stay below
+  // 2^kLazyLog2 and the accumulator is rescaled only on those tiles.
+  float m_ref = -INFINITY, l_run = 0.f;   // l_run: this lane's half of the row sum
+  const float c = p.scale_log2;
+  const float thr = kLazyLog2 / c;
+
+  // Softmax of one tile in place (st becomes P); returns whether the
+  // reference max moved, with the accumulator factor in `alpha`.
+  auto softmax = [&](f32x16 (&st)[2], float& alpha) {
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[t][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
+    mx = xhalf_max(mx);
+    const bool raise = __builtin_amdgcn_ballot_w64(mx > m_ref + thr) != 0;
+    const float m_new = raise ? fmaxf(m_ref, mx) : m_ref;
     const float mc = (m_new == -INFINITY) ? 0.f : m_new * c;
-    const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
+    alpha = raise ? __builtin_amdgcn_exp2f(fmaf(m_ref, c, -mc)) : 1.f;
+    m_ref = m_new;
     float rs = 0.f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -179,12 +209,11 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
         st[t][r] = e;
         rs += e;
       }
-    rs += __shfl_xor(rs, 32, 64);
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < D / 32; ++t) oacc[t] *= alpha;
-
+    l_run = fmaf(l_run, alpha, rs);
+    return raise;
+  };
+  auto pv = [&](int buf, const f32x16 (&st)[2]) {
+    const uint16_t* Vb = Vt[buf] + l32 * VROW + g * 4;
 #pragma unroll
     for (int cc = 0; cc < KB / 16; ++cc) {
       const int t = cc >> 1, base = (cc & 1) * 8;
@@ -194,23 +223,79 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
       const bf16x8 pb = __builtin_bit_cast(bf16x8, pk);
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        const uint16_t* vrow = &Vb[(dt * 32 + l32) * VROW + cc * 16 + g * 4];
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 8);
+        // keys cc*16 + g*4 + {0..3} and + 8, at their swizzled slots (dv / 32 == dt)
+        const uint16_t* vrow = Vb + dt * 32 * VROW;
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + ((cc * 16) ^ (8 * dt)));
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + ((cc * 16 + 8) ^ (8 * dt)));
         const u32x4 av = {lo.x, lo.y, hi.x, hi.y};
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pb,
                                                            oacc[dt], 0, 0, 0);
       }
     }
-    // Stage tile kt+1 (loaded during this tile) and start loading kt+2.
-    if (kt + 1 < ntiles) {
-      swrite(buf ^ 1);
-      if (kt + 2 < ntiles) gload((kt + 2) * KB);
-    }
+  };
+  auto rescale = [&](float alpha) {
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) oacc[t] *= alpha;
+  };
+
+  // Pipeline: while tile j's softmax runs, tile j+1's scores are computed
+  // from its K tile (already in LDS); K is staged two tiles ahead, V one.
+  gload(skr, kbase, 0);
+  gload(svr, vbase, 0);
+  swriteK(0);
+  swriteV(0);
+  if (ntiles > 1) {
+    gload(skr, kbase, KB);
+    swriteK(1);
+    gload(svr, vbase, KB);
+  }
+  if (ntiles > 2) gload(skr, kbase, 2 * KB);
+  barrier();
+  // One pipeline step: scores of tile j+1 into `nxt` while tile j (scores in
+  // `cur`, wholly below the diagonal) goes through softmax and PV.
+  auto step = [&](int j, f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+    barrier();   // K_{j+1} and V_j resident; the buffers of K_j and V_{j-1} free
+    scores((j + 1) & 1, nxt);
+    float alpha;
+    if (softmax(cur, alpha)) rescale(alpha);
+    pv(j & 1, cur);
+    if (j + 2 < ntiles) swriteK(j & 1);
+    swriteV((j + 1) & 1);
+    if (j + 3 < ntiles) gload(skr, kbase, (j + 3) * KB);
+    if (j + 2 < ntiles) gload(svr, vbase, (j + 2) * KB);
+  };
+  f32x16 sa[2], sb[2];
+  scores(0, sa);
+  int j = 0;
+  for (; j + 2 < ntiles; j += 2) {
+    step(j, sa, sb);
+    step(j + 1, sb, sa);
+  }
+  if (j + 1 < ntiles) {
+    step(j, sa, sb);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) sa[t] = sb[t];
+  }
+  f32x16 (&st)[2] = sa;
+  {
+    // Last tile: it holds the diagonal and the sequence end.
+    const int k0 = (ntiles - 1) * KB;
+    barrier();
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + t * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+        if (key > qpos || key >= len) st[t][r] = -INFINITY;
+      }
+    float alpha;
+    if (softmax(st, alpha)) rescale(alpha);
+    pv((ntiles - 1) & 1, st);
   }
 
+  const float l_tot = xhalf_sum(l_run);
   if (!qvalid) return;
-  const float inv_l = l_run > 0.f ? 1.f / l_run : 0.f;
+  const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
   uint16_t* orow = p.o + (static_cast<int64_t>(row0 + qpos) * p.Hq + h) * D;
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt)
@@ -303,7 +388,7 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
   __syncthreads();
   // Per-head max and sum over the split: wave w owns heads w, w + 4.
   {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     for (int g = wave; g < G; g += kDecThreads / 64) {
       const float v = sc[g][lane];
       const float m = wave_max(v);
@@ -412,21 +497,26 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnParams p, Ro
 hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipStream_t s) {
   AttnSched sch;
   sch.prefix[0] = 0;
+  int maxlen = 0;
   for (int i = 0; i < rm.n_seqs; ++i) {
     const int len = rm.cu[i + 1] - rm.cu[i];
+    maxlen = std::max(maxlen, len);
     sch.prefix[i + 1] = sch.prefix[i] + (len + QB - 1) / QB;
   }
   sch.total = sch.prefix[rm.n_seqs];
   if (sch.total == 0) return hipSuccess;
   const int G = p.Hq / p.Hkv;
+  if (maxlen > kMaxPrefillLen || p.page != kPage) return hipErrorInvalidValue;
   dim3 grid(sch.total, p.Hkv);
-#define PALLAS_ATTN_CASE(DD, GG) \
-  if (p.d == DD && G == GG) { attn_prefill_kernel<DD, GG><<<grid, GG * 64, 0, s>>>(p, rm, sch); return hipGetLastError(); }
+#define PALLAS_ATTN_CASE(DD, GG)                                                        \
+  if (p.d == DD && G == GG) {                                                           \
+    attn_prefill_kernel<DD, GG><<<grid, GG * 64, 0, s>>>(p, rm, sch);                   \
+    return hipGetLastError();                                                           \
+  }
   PALLAS_ATTN_CASE(128, 1) PALLAS_ATTN_CASE(128, 2) PALLAS_ATTN_CASE(128, 4) PALLAS_ATTN_CASE(128, 8)
   PALLAS_ATTN_CASE(64, 1) PALLAS_ATTN_CASE(64, 2) PALLAS_ATTN_CASE(64, 4) PALLAS_ATTN_CASE(64, 8)
 #undef PALLAS_ATTN_CASE
   return hipErrorInvalidValue;
-  return hipGetLastError();
 }
 
 hipError_t launch_attention_decode(const AttnParams& p, const RowMap& rm, float* partial,

@@ -68,6 +68,7 @@ namespace pallas {
 
 // ------------------------------------------------------------ row metadata
 constexpr int kMaxSeqs = 64;
+constexpr int kMaxPrefillLen = 32768;  // tokens per sequence in one prefill call
 
 // Rows [cu[s], cu[s+1]) belong to sequence s and sit at positions
 // base_pos[s] + (row - cu[s]); sequence s uses block-table row s.

@@ -12,6 +12,9 @@
 #include "pallas.h"
 #include "kernels.h"
 #include "model_plan.h"
+
+static_assert(PALLAS_MAX_SEQS == pallas::kMaxSeqs, "sequence limit");
+static_assert(PALLAS_MAX_PREFILL_LEN == pallas::kMaxPrefillLen, "prefill length limit");
 #include "profile.h"
 
 namespace {
@@ -502,6 +505,9 @@ int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_to
     if (len > cap)
       return fail(PALLAS_ERR_OUT_OF_RANGE, "prefill: sequence %d of %lld tokens exceeds the table (%lld)", i,
                   (long long)len, (long long)cap);
+    if (len > PALLAS_MAX_PREFILL_LEN)
+      return fail(PALLAS_ERR_UNSUPPORTED, "prefill: sequence %d of %lld tokens (at most %d per call)", i,
+                  (long long)len, PALLAS_MAX_PREFILL_LEN);
     rm.base_pos[i] = 0;
   }
   const int64_t M = h_cu_seqlens[num_seqs];

@@ -130,3 +130,33 @@ def test_model_create_rejects_bad_shapes(P):
     assert rc(head_dim=96) == P.Status.UNSUPPORTED
     assert rc(page_size=32) == P.Status.UNSUPPORTED
     assert rc(hidden=200) == P.Status.UNSUPPORTED
+
+
+def test_prefill_rejects_sequences_beyond_the_length_limit(P):
+    """A sequence longer than PALLAS_MAX_PREFILL_LEN tokens is refused on the
+    host (UNSUPPORTED) before anything touches the device; one at the limit
+    passes that check and stops at the (undersized) workspace instead."""
+    from workloads import configs
+    from paper_2608_16477_amd.binding import ModelConfigC, WeightsC, LayerWeightsC, KVPoolC
+    h = P.lib()
+    c = configs.TINY
+    cc = ModelConfigC(c.n_layers, c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn,
+                      c.vocab, c.rms_eps, c.rope_theta, int(c.qk_norm), c.page_size)
+    la = (LayerWeightsC * c.n_layers)()
+    for l in range(c.n_layers):
+        for name, _ in LayerWeightsC._fields_:
+            setattr(la[l], name, FAKE)
+    w = WeightsC(FAKE, FAKE, FAKE, la)
+    model = C.c_void_p()
+    assert h.pallas_model_create(C.byref(cc), C.byref(w), C.byref(model)) == 0
+    limit = 32768
+    pool = KVPoolC(FAKE, 4096, c.page_size, c.n_layers, c.n_kv_heads, c.head_dim)
+    try:
+        def rc(n):
+            cu = (C.c_int32 * 2)(0, n)
+            return P.Status(h.pallas_prefill_prefix(model, 1, FAKE, cu, FAKE, 4096, C.byref(pool),
+                                                    FAKE, 256, None, None))
+        assert rc(limit + 1) == P.Status.UNSUPPORTED
+        assert rc(limit) == P.Status.WORKSPACE
+    finally:
+        h.pallas_model_destroy(model)
