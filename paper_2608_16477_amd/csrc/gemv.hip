@@ -1,10 +1,15 @@
 // Skinny GEMM for decode (M <= 8 rows): C = X W^T streaming the weights once.
 //
-// A workgroup of 8 waves owns two 16-column tiles of W and splits K eight
-// ways; each wave runs v_mfma_f32_16x16x32_bf16 with X (rows padded to 16
-// with zeros) as the A operand and 16 weight rows, loaded straight from
-// memory in operand layout, as the B operand.  The eight partial tiles are
-// summed through LDS and the epilogue matches the prefill GEMM's.
+// A workgroup of 8 waves owns one 16-row weight tile (two for the gate|up
+// projection: 16 gate rows and the matching 16 up rows) and splits K eight
+// ways.  Each wave streams its K range in steps of 64: one 128-byte line of
+// each weight row and the matching 64 columns of X go straight from memory
+// into a private LDS stage with buffer_load ... lds (three stages in
+// flight), each load instruction covering whole lines of 8 rows.  Inside a
+// stage the 16-byte slots are permuted so the v_mfma_f32_16x16x32_bf16
+// operand reads (16 rows at one k) hit 16 distinct bank groups.  The eight
+// partial tiles are summed through LDS and the epilogue matches the prefill
+// GEMM's.
 #include "common.h"
 #include "kernels.h"
 
@@ -14,66 +19,134 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kUnroll = 4;
+constexpr int kStages = 3;
+constexpr int kKStep = 64;        // k per stage: one 128-byte line per weight row
+constexpr int kBlockSlots = 68;   // 8 rows x 8 slots of 16 B, plus 4 slots of padding
 
-template <int EPI>
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int TILES>
+struct GvLayout {
+  static constexpr int kWBlocks = 2 * TILES;                          // 8-row blocks per stage
+  static constexpr int kStageSlots = kWBlocks * kBlockSlots + 64;     // + one X block
+  static constexpr int kWaveSlots = kStages * kStageSlots;
+  static constexpr int kLoads = kWBlocks + 1;                         // load instructions per stage
+};
+
+// Weight block slot of (row rr in 0..7, 16-byte chunk c in 0..7).
+__device__ __forceinline__ int wslot(int rr, int c) {
+  return (rr & 3) + 8 * (rr >> 2) + 4 * (c & 1) + 16 * (c >> 1);
+}
+// X block slot of (row r in 0..7, chunk c in 0..7).
+__device__ __forceinline__ int xslot(int r, int c) { return r * 8 + (c ^ r); }
+
+template <int EPI, int TILES>
 __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restrict__ X, int ldx,
                                                         const uint16_t* __restrict__ W, int ldw,
                                                         void* __restrict__ C, int ldc, int M, int N,
-                                                        int K, int w_rows) {
-  __shared__ f32x4 red[kWaves][2][64];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+                                                        int K) {
+  using L = GvLayout<TILES>;
+  __shared__ __attribute__((aligned(16))) u32x4 lds[kWaves * L::kWaveSlots];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, kg = lane >> 4;
-  // weight rows of the two tiles
-  int wrow[2];
+
+  // Weight tiles: first row and valid row count.
+  int trow[TILES], tvalid[TILES];
   if (EPI == kEpiSwiGLU) {
-    const int o = blockIdx.x * 16 + li;
-    wrow[0] = o < N ? o : -1;
-    wrow[1] = o < N ? N + o : -1;
+    const int o0 = blockIdx.x * 16;
+    trow[0] = o0;
+    trow[TILES - 1] = N + o0;
+    tvalid[0] = tvalid[TILES - 1] = min(16, N - o0);
   } else {
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int n = blockIdx.x * 32 + t * 16 + li;
-      wrow[t] = n < N ? n : -1;
+    for (int t = 0; t < TILES; ++t) {
+      trow[t] = (blockIdx.x * TILES + t) * 16;
+      tvalid[t] = max(0, min(16, N - trow[t]));
     }
   }
-  (void)w_rows;
-  const int kslice = ((K + kWaves * 32 - 1) / (kWaves * 32)) * 32;
-  const int kb = wave * kslice, ke = min(K, kb + kslice);
-  const bool xrow_ok = li < M;
-  const uint16_t* xr = X + static_cast<int64_t>(xrow_ok ? li : 0) * ldx;
-  const uint16_t* wr0 = W + static_cast<int64_t>(wrow[0] < 0 ? 0 : wrow[0]) * ldw;
-  const uint16_t* wr1 = W + static_cast<int64_t>(wrow[1] < 0 ? 0 : wrow[1]) * ldw;
+  auto tile_rsrc = [&](int t) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(W + static_cast<int64_t>(tvalid[t] > 0 ? trow[t] : 0) * ldw), 0,
+                                             static_cast<uint32_t>(tvalid[t]) * ldw * 2u, 0x00020000);
+  };
+  const __amdgpu_buffer_rsrc_t rw0 = tile_rsrc(0), rw1 = tile_rsrc(TILES - 1);
+  const __amdgpu_buffer_rsrc_t rx =
+      __builtin_amdgcn_make_buffer_rsrc((void*)X, 0, static_cast<uint32_t>(M) * ldx * 2u, 0x00020000);
+  constexpr uint32_t kOob = 0xFFFFFFF0u;
 
-  f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-  for (int k = kb; k < ke; k += 32 * kUnroll) {
-    u32x4 xa[kUnroll], w0[kUnroll], w1[kUnroll];
+  const int kslice = ((K + kWaves * kKStep - 1) / (kWaves * kKStep)) * kKStep;
+  const int kb = wave * kslice, ke = min(K, kb + kslice);
+  const int nst = ke > kb ? (ke - kb + kKStep - 1) / kKStep : 0;
+
+  // Per-lane load coordinates (fixed for every stage).
+  // Weight block instruction: lane -> slot lane -> (row rr, chunk c).
+  const int b = lane & 15;
+  const int w_rr = (b & 3) | ((b >> 3) << 2);
+  const int w_c = ((lane >> 4) << 1) | ((b >> 2) & 1);
+  // X block instruction: lane -> row lane/8, chunk (lane%8) ^ row.
+  const int x_r = lane >> 3;
+  const int x_c = (lane & 7) ^ x_r;
+
+  u32x4* wbase = lds + wave * L::kWaveSlots;
+  auto issue = [&](int s) {
+    const int k0 = kb + s * kKStep;
+    u32x4* st = wbase + (s % kStages) * L::kStageSlots;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int kk = k + u * 32 + kg * 8;
-      const bool ok = kk < ke;
-      xa[u] = (ok && xrow_ok) ? *reinterpret_cast<const u32x4*>(xr + kk) : u32x4{0, 0, 0, 0};
-      w0[u] = (ok && wrow[0] >= 0) ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wr0 + kk))
-                                   : u32x4{0, 0, 0, 0};
-      w1[u] = (ok && wrow[1] >= 0) ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wr1 + kk))
-                                   : u32x4{0, 0, 0, 0};
+    for (int blk = 0; blk < L::kWBlocks; ++blk) {
+      const int t = blk >> 1;
+      const int row = (blk & 1) * 8 + w_rr;
+      const int k = k0 + w_c * 8;
+      const uint32_t off = k < ke ? static_cast<uint32_t>(row) * ldw * 2u + static_cast<uint32_t>(k) * 2u : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(t == 0 ? rw0 : rw1, (lds_void*)(st + blk * kBlockSlots), 16, off, 0, 0, 0);
     }
+    const int k = k0 + x_c * 8;
+    const uint32_t off = (x_r < M && k < ke) ? static_cast<uint32_t>(x_r) * ldx * 2u + static_cast<uint32_t>(k) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)(st + L::kWBlocks * kBlockSlots), 16, off, 0, 0, 0);
+  };
+
+  f32x4 acc[TILES];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const bf16x8 a = __builtin_bit_cast(bf16x8, xa[u]);
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, w0[u]), acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, w1[u]), acc1, 0, 0, 0);
+  for (int t = 0; t < TILES; ++t) acc[t] = f32x4{0, 0, 0, 0};
+  auto compute = [&](int s) {
+    const u32x4* st = wbase + (s % kStages) * L::kStageSlots;
+#pragma unroll
+    for (int q = 0; q < kKStep / 32; ++q) {
+      const int c = 4 * q + kg;
+      const bf16x8 a = __builtin_bit_cast(bf16x8, st[L::kWBlocks * kBlockSlots + xslot(li & 7, c)]);
+#pragma unroll
+      for (int t = 0; t < TILES; ++t) {
+        const bf16x8 w = __builtin_bit_cast(bf16x8, st[(2 * t + (li >> 3)) * kBlockSlots + wslot(li & 7, c)]);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w, acc[t], 0, 0, 0);
+      }
     }
+  };
+
+  for (int s = 0; s < kStages - 1 && s < nst; ++s) issue(s);
+  for (int s = 0; s < nst; ++s) {
+    asm volatile("" ::: "memory");
+    if (s + kStages - 1 < nst) {
+      issue(s + kStages - 1);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kStages - 1) * L::kLoads) : "memory");
+    } else if (s + 1 < nst) {
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L::kLoads) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    compute(s);
   }
-  red[wave][0][lane] = acc0;
-  red[wave][1][lane] = acc1;
+
+  // Sum the eight partial tiles.
+  __syncthreads();
+  f32x4* red = reinterpret_cast<f32x4*>(lds);
+#pragma unroll
+  for (int t = 0; t < TILES; ++t) red[(wave * TILES + t) * 64 + lane] = acc[t];
   __syncthreads();
   if (wave != 0) return;
-  f32x4 s0 = red[0][0][lane], s1 = red[0][1][lane];
+  f32x4 sum[TILES];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) {
-    s0 += red[w][0][lane];
-    s1 += red[w][1][lane];
+  for (int t = 0; t < TILES; ++t) {
+    sum[t] = red[t * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) sum[t] += red[(w * TILES + t) * 64 + lane];
   }
   // lane holds column li and rows kg*4 + r
 #pragma unroll
@@ -83,15 +156,15 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
     if (EPI == kEpiSwiGLU) {
       const int col = blockIdx.x * 16 + li;
       if (col < N) {
-        const float gt = s0[r], up = s1[r];
+        const float gt = sum[0][r], up = sum[TILES - 1][r];
         static_cast<uint16_t*>(C)[static_cast<int64_t>(m) * ldc + col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
       }
     } else {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int col = blockIdx.x * 32 + t * 16 + li;
+      for (int t = 0; t < TILES; ++t) {
+        const int col = trow[t] + li;
         if (col >= N) continue;
-        const float v = t == 0 ? s0[r] : s1[r];
+        const float v = sum[t][r];
         const int64_t at = static_cast<int64_t>(m) * ldc + col;
         if (EPI == kEpiBf16) static_cast<uint16_t*>(C)[at] = f2bf(v);
         else if (EPI == kEpiAddF32) static_cast<float*>(C)[at] += v;
@@ -105,13 +178,16 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
 
 hipError_t launch_gemv(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
                        int ldc, int M, int N, int K, hipStream_t s) {
-  if (M <= 0 || M > 8) return hipErrorInvalidValue;
-  const int w_rows = epi == kEpiSwiGLU ? 2 * N : N;
+  if (M <= 0 || M > 8 || N <= 0 || K <= 0 || (K & 7) || (lda & 7) || (ldb & 7)) return hipErrorInvalidValue;
+  // 32-bit buffer offsets: one 16-row weight tile and the X rows
+  if (static_cast<int64_t>(16) * ldb * 2 >= (int64_t(1) << 32) || static_cast<int64_t>(8) * lda * 2 >= (int64_t(1) << 32))
+    return hipErrorInvalidValue;
+  const int tiles = (N + 15) / 16;
   switch (epi) {
-    case kEpiBf16: gemv_kernel<kEpiBf16><<<(N + 31) / 32, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, w_rows); break;
-    case kEpiAddF32: gemv_kernel<kEpiAddF32><<<(N + 31) / 32, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, w_rows); break;
-    case kEpiF32: gemv_kernel<kEpiF32><<<(N + 31) / 32, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, w_rows); break;
-    case kEpiSwiGLU: gemv_kernel<kEpiSwiGLU><<<(N + 15) / 16, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, w_rows); break;
+    case kEpiBf16: gemv_kernel<kEpiBf16, 1><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
+    case kEpiAddF32: gemv_kernel<kEpiAddF32, 1><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
+    case kEpiF32: gemv_kernel<kEpiF32, 1><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
+    case kEpiSwiGLU: gemv_kernel<kEpiSwiGLU, 2><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
