@@ -71,6 +71,8 @@ def parse():
                     choices=["tiny", "mid", "large", "large-aligned", "concurrent"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stress", action="store_true",
+                    help="skip the stress-layout copy measurements (suffixes of 64-4096 tokens)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device-to-device copy and exit (the reference "
                          "point for scaling FETCH_SIZE / WRITE_SIZE counter readings)")
@@ -173,6 +175,75 @@ class Setup:
 
     def decode(self):
         self.model.decode_step(self.tokens, self.ns, self.dst_tab, self.dst, self.logits, self.ws, self.err)
+
+
+def copies_stress(P, seed):
+    """Pack and assemble at the stress layout: an 8192-token source of
+    N(0,1) K/V in 512 shuffled pages, a 1024-page target pool with half its
+    pages occupied, suffixes of 64-4096 tokens moved as in-order 32-token
+    chunks, all chunks of one suffix in one launch.  Ten warm-up calls, then
+    the median of 50 event-timed calls per figure; one more row times one
+    launch per 32-token chunk."""
+    import numpy as np
+    import torch
+    from workloads import configs, gen
+
+    cfg = configs.STRESS_KV
+    L, hkv, d = cfg.n_layers, cfg.n_kv_heads, cfg.head_dim
+    n_src = configs.STRESS_SOURCE_TOKENS
+    src_pages = n_src // cfg.page_size
+    tp = configs.STRESS_TARGET_PAGES
+    src = gen.kv_pool_normal(L, src_pages, cfg.page_size, hkv, d, seed=seed, device="cuda")
+    src_bt = torch.from_numpy(gen.block_table(src_pages, src_pages, src_pages, seed, 1)).cuda()
+    occupied = np.sort(gen.permutation(tp, seed, 2)[: tp // 2])
+    free = np.setdiff1d(np.arange(tp), occupied).astype(np.int32)
+    dst = torch.empty((L, 2, tp, cfg.page_size, hkv, d), dtype=torch.bfloat16, device="cuda")
+    dst.view(torch.int16).fill_(gen.SENTINEL_BITS)
+    dst_bt = torch.from_numpy(gen.block_table(src_pages, tp, src_pages, seed, 3, free_pages=free)).cuda()
+    row = cfg.s_kv
+    arena = torch.empty(max(configs.STRESS_SUFFIXES) * row, dtype=torch.uint8, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def median_us(fn, reps=50, warm=10):
+        for _ in range(warm):
+            fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for a, b in evs:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3
+
+    rows = []
+    for s in configs.STRESS_SUFFIXES:
+        start = n_src - s
+        descs, hdrs = [], []
+        for k, t in enumerate(range(start, n_src, configs.STRESS_CHUNK)):
+            c = min(configs.STRESS_CHUNK, n_src - t)
+            descs.append(P.ChunkDesc(t, c, k * configs.STRESS_CHUNK * row))
+            hdrs.append(P.ChunkHeader(7, 1, t, c, k * configs.STRESS_CHUNK * row, L, hkv, d, 2))
+        nbytes = 2 * s * row
+        t_pack = median_us(lambda: P.pallas_pack_suffix_blocks(src, src_bt, descs, arena, err))
+        t_asm = median_us(lambda: P.pallas_assemble_kv(dst, dst_bt, hdrs, arena, 7, 1, err))
+        rows.append({"suffix_tokens": s, "chunks_per_launch": len(descs), "bytes": nbytes,
+                     "pack_us": t_pack, "pack_GBps": nbytes / t_pack / 1e3,
+                     "pack_hbm_frac": nbytes / t_pack / 1e3 / PEAK_HBM_GBPS,
+                     "assemble_us": t_asm, "assemble_GBps": nbytes / t_asm / 1e3,
+                     "assemble_hbm_frac": nbytes / t_asm / 1e3 / PEAK_HBM_GBPS})
+    # one launch per 32-token chunk
+    c = configs.STRESS_CHUNK
+    one_d = [P.ChunkDesc(n_src - c, c, 0)]
+    one_h = [P.ChunkHeader(7, 1, n_src - c, c, 0, L, hkv, d, 2)]
+    lat = {"chunk_tokens": c, "bytes": 2 * c * row,
+           "pack_us": median_us(lambda: P.pallas_pack_suffix_blocks(src, src_bt, one_d, arena, err)),
+           "assemble_us": median_us(lambda: P.pallas_assemble_kv(dst, dst_bt, one_h, arena, 7, 1, err))}
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0, "device-side error flag raised in the stress copies"
+    return {"layout": (f"{L} layers, {hkv} KV heads, head_dim {d}: {n_src}-token source in "
+                       f"{src_pages} shuffled pages; {tp}-page target, half occupied; "
+                       f"{c}-token chunks"), "rows": rows, "per_chunk_launch": lat}
 
 
 def cpu_baseline(setup):
@@ -341,6 +412,9 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if not args.no_stress:
+        print("[bench] stress-layout copies", file=sys.stderr, flush=True)
+        out["copies_stress"] = copies_stress(P, args.seed)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(st)
