@@ -1,7 +1,8 @@
 """GPU parity of suffix-block extraction (pack) and assembly against the
 oracle: bit-exact on every element, including untouched pages and slots.
 
-Cases: a tiny pool with ragged, unaligned and empty chunks; the 64-layer /
+Cases: a tiny pool with ragged, unaligned and empty chunks; page sizes 4,
+8 and 32 (shorter and longer than a 16-position work unit); the 64-layer /
 8-KV-head / d=128 stress layout (8192-token source in shuffled pages, a
 1024-page target half occupied by sentinel pages, suffixes of 64, 256, 1024
 and 4096 tokens in 32-token chunks); invalid table entries; rejected calls."""
@@ -67,6 +68,35 @@ def test_tiny_ragged_chunks(P):
         np.testing.assert_array_equal(arena_chunk(arena, off, c, L, hkv, d), want)
         hdrs.append(paged.ChunkHeader(1, 1, s, c, L, hkv, d, 2))
     chunks = [paged.pack(src_np, src_bt.numpy(), s, c) for s, c, _ in lay]
+    assert paged.assemble(dst_np, dst_bt.numpy(), hdrs, chunks, 1, 1)
+    np.testing.assert_array_equal(bits(dst_gpu), dst_np)
+
+
+@pytest.mark.parametrize("page", [4, 8, 32])
+def test_other_page_sizes_bit_exact(P, page):
+    """Pages shorter than a 16-position run (each position looks up its own
+    page) and longer ones (a run spans at most two pages), with unaligned
+    and ragged chunks."""
+    L, hkv, d = 2, 2, 64
+    n_src = 8 * 32
+    pages = n_src // page
+    src = gen.kv_pool_normal(L, pages, page, hkv, d, seed=12)
+    src_bt = torch.from_numpy(gen.block_table(pages, pages, pages, 12, 1))
+    dst_pages = 2 * pages
+    dst = torch.empty((L, 2, dst_pages, page, hkv, d), dtype=torch.bfloat16)
+    dst.view(torch.int16).fill_(gen.SENTINEL_BITS)
+    dst_bt = torch.from_numpy(gen.block_table(pages, dst_pages, pages, 12, 2))
+    pieces = [(3, 29), (32, 1), (33, 70), (103, 16), (119, n_src - 119)]
+    src_np, dst_np = bits(src), bits(dst)
+    arena, lay, err = run_pack_assemble(P, src.to(DEV), src_bt.to(DEV), dst_gpu := dst.to(DEV),
+                                        dst_bt.to(DEV), pieces)
+    assert err == 0
+    hdrs, chunks = [], []
+    for s0, c, off in lay:
+        want = paged.pack(src_np, src_bt.numpy(), s0, c)
+        np.testing.assert_array_equal(arena_chunk(arena, off, c, L, hkv, d), want)
+        hdrs.append(paged.ChunkHeader(1, 1, s0, c, L, hkv, d, 2))
+        chunks.append(want)
     assert paged.assemble(dst_np, dst_bt.numpy(), hdrs, chunks, 1, 1)
     np.testing.assert_array_equal(bits(dst_gpu), dst_np)
 
