@@ -312,83 +312,119 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
 constexpr int kDecThreads = 256;
 constexpr int kDecSplit = 64;   // keys per split
 constexpr int kMaxG = 8;
+constexpr int kDecMaxSplitsLds = 1024;   // split records staged in LDS by the combine pass
 
 // Decode attention, split over keys: workgroup (split of 64 keys, KV head,
-// seq) scores its keys for all G query heads of the KV head (4 threads per
-// key, each over a quarter of the head dimension, so every K row is read
-// once), keeps the split's max, sum and unnormalised output per head in the
-// partial buffer; decode_combine merges the splits.
+// seq).  Every K and V row of the split and the G query rows are loaded into
+// LDS at once (one table read and one 16-byte load per row chunk and
+// thread, all in flight together); then scores (4 threads per key, a
+// quarter of the head dimension each), the per-head max and sum over the
+// split, and PV (each thread a few output dimensions of one head) run from
+// LDS.  The partial record per (seq, head, split) is [max, sum, o[0..d)];
+// decode_combine merges the splits.
 template <int D>
 __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnParams p, RowMap rm,
                                                                         float* __restrict__ part,
                                                                         int max_splits) {
-  constexpr int TPK = kDecThreads / kDecSplit;  // threads per key (4)
-  constexpr int DPT = D / TPK;                  // dimensions per thread
-  constexpr int NG = kDecThreads / D;           // key groups in the PV pass
-  constexpr int KPG = kDecSplit / NG;           // keys per group
-  __shared__ float qs[kMaxG][D];
+  constexpr int CH = D / 8;                        // 16-byte chunks per row
+  constexpr int RPP = kDecThreads / CH;            // rows loaded per pass
+  constexpr int NPASS = kDecSplit / RPP;           // load passes
+  constexpr int KROW = D + 8;                      // padded LDS row (elements)
+  constexpr int TPK = kDecThreads / kDecSplit;     // threads per key in the score pass
+  constexpr int DPT = D / TPK;                     // dimensions per score thread
+  constexpr int OPT = kMaxG * D / kDecThreads;     // PV outputs per thread
+  constexpr int TPH = D / OPT;                     // PV threads per head
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kDecSplit * KROW];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[kDecSplit * KROW];
+  __shared__ __attribute__((aligned(16))) float qs[kMaxG][D];
   __shared__ float sc[kMaxG][kDecSplit];
   __shared__ float stat[kMaxG][2];
-  __shared__ float oacc[NG][kMaxG][D];
+  __shared__ int kok[kDecSplit];
   const int G = p.Hq / p.Hkv;
   const int split = blockIdx.x, kh = blockIdx.y, s = blockIdx.z;
   const int n = rm.base_pos[s];
   const int j0 = split * kDecSplit;
   if (j0 > n) return;
-  const int jn = min(n + 1 - j0, kDecSplit);
+  const int jn = min(n + 1 - j0, kDecSplit);   // keys of this split at positions <= n
   const int row = rm.cu[s];
   const int32_t* bt = p.bt + static_cast<int64_t>(s) * p.max_pages;
-  for (int i = threadIdx.x; i < G * D; i += kDecThreads)
-    qs[i / D][i % D] = bf2f(p.q[(static_cast<int64_t>(row) * p.Hq + kh * G + i / D) * D + i % D]);
+  const int t = threadIdx.x;
+
+  {
+    // Keys past jn read key jn - 1 (their scores are masked); rows on a page
+    // outside the pool load zeros and are masked.
+    const int ch = t % CH, r0 = t / CH;
+    u32x4 kv[NPASS], vv[NPASS];
+    bool ok[NPASS];
+#pragma unroll
+    for (int i = 0; i < NPASS; ++i) {
+      const int j = j0 + min(r0 + i * RPP, jn - 1);
+      const int pg = bt[j / p.page];
+      ok[i] = pg >= 0 && pg < p.num_pages;
+      const int64_t off = ((static_cast<int64_t>(ok[i] ? pg : 0) * p.page + j % p.page) * p.Hkv + kh) * D + ch * 8;
+      kv[i] = ok[i] ? *reinterpret_cast<const u32x4*>(p.k_plane + off) : u32x4{0, 0, 0, 0};
+      vv[i] = ok[i] ? *reinterpret_cast<const u32x4*>(p.v_plane + off) : u32x4{0, 0, 0, 0};
+    }
+    const int qg = t / CH;
+    u32x4 qv = {0, 0, 0, 0};
+    if (qg < G) qv = *reinterpret_cast<const u32x4*>(p.q + (static_cast<int64_t>(row) * p.Hq + kh * G + qg) * D + ch * 8);
+#pragma unroll
+    for (int i = 0; i < NPASS; ++i) {
+      const int r = r0 + i * RPP;
+      *reinterpret_cast<u32x4*>(&Ks[r * KROW + ch * 8]) = kv[i];
+      *reinterpret_cast<u32x4*>(&Vs[r * KROW + ch * 8]) = vv[i];
+      if (ch == 0) kok[r] = ok[i] && r < jn;
+    }
+    if (qg < kMaxG) {
+      float4* qd = reinterpret_cast<float4*>(&qs[qg][ch * 8]);
+      qd[0] = float4{bflo(qv[0]), bfhi(qv[0]), bflo(qv[1]), bfhi(qv[1])};
+      qd[1] = float4{bflo(qv[2]), bfhi(qv[2]), bflo(qv[3]), bfhi(qv[3])};
+    }
+  }
   __syncthreads();
 
-  // Scores: thread (key, quarter).
-  const int key = threadIdx.x / TPK, qt = threadIdx.x % TPK;
-  float acc[kMaxG];
+  {
+    // Scores: thread (key, part of the head dimension).
+    const int key = t / TPK, qt = t % TPK;
+    float acc[kMaxG];
 #pragma unroll
-  for (int g = 0; g < kMaxG; ++g) acc[g] = 0.f;
-  bool valid = false;
-  if (key < jn) {
-    const int j = j0 + key;
-    const int pg = bt[j / p.page];
-    if (pg >= 0 && pg < p.num_pages) {
-      valid = true;
-      const uint16_t* k = p.k_plane + ((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D + qt * DPT;
-      u32x4 w[DPT / 8];
+    for (int g = 0; g < kMaxG; ++g) acc[g] = 0.f;
+    const uint16_t* kr = &Ks[key * KROW + qt * DPT];
 #pragma unroll
-      for (int c = 0; c < DPT / 8; ++c) w[c] = *reinterpret_cast<const u32x4*>(k + c * 8);
+    for (int c = 0; c < DPT / 8; ++c) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(kr + c * 8);
+      float kf[8];
 #pragma unroll
-      for (int c = 0; c < DPT / 8; ++c) {
-        float kf[8];
+      for (int e = 0; e < 4; ++e) {
+        kf[2 * e] = bflo(w[e]);
+        kf[2 * e + 1] = bfhi(w[e]);
+      }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          kf[2 * e] = bflo(w[c][e]);
-          kf[2 * e + 1] = bfhi(w[c][e]);
-        }
-#pragma unroll
-        for (int g = 0; g < kMaxG; ++g) {
-          if (g < G) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[g] += qs[g][qt * DPT + c * 8 + e] * kf[e];
-          }
+      for (int g = 0; g < kMaxG; ++g) {
+        if (g < G) {
+          const float4* q4 = reinterpret_cast<const float4*>(&qs[g][qt * DPT + c * 8]);
+          const float4 a = q4[0], b = q4[1];
+          acc[g] += a.x * kf[0] + a.y * kf[1] + a.z * kf[2] + a.w * kf[3] +
+                    b.x * kf[4] + b.y * kf[5] + b.z * kf[6] + b.w * kf[7];
         }
       }
     }
-  }
 #pragma unroll
-  for (int g = 0; g < kMaxG; ++g) {
-    acc[g] += __shfl_xor(acc[g], 1, kWave);
-    acc[g] += __shfl_xor(acc[g], 2, kWave);
-  }
-  if (qt == 0 && key < kDecSplit) {
+    for (int g = 0; g < kMaxG; ++g) {
 #pragma unroll
-    for (int g = 0; g < kMaxG; ++g)
-      if (g < G) sc[g][key] = valid ? acc[g] * p.scale_log2 : -INFINITY;
+      for (int o = 1; o < TPK; o <<= 1) acc[g] += __shfl_xor(acc[g], o, kWave);
+    }
+    if (qt == 0) {
+      const bool valid = kok[key] != 0;
+#pragma unroll
+      for (int g = 0; g < kMaxG; ++g)
+        if (g < G) sc[g][key] = valid ? acc[g] * p.scale_log2 : -INFINITY;
+    }
   }
   __syncthreads();
-  // Per-head max and sum over the split: wave w owns heads w, w + 4.
   {
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    // Per-head max and sum over the split: wave w owns heads w, w + 4.
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6), lane = t & 63;
     for (int g = wave; g < G; g += kDecThreads / 64) {
       const float v = sc[g][lane];
       const float m = wave_max(v);
@@ -402,46 +438,32 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
     }
   }
   __syncthreads();
-  // Weighted sum of V: thread (dim dv, key group kg), eight V loads in flight.
-  const int dv = threadIdx.x % D, kg = threadIdx.x / D;
-  float o[kMaxG];
+  {
+    // PV: thread (head g, OPT consecutive output dimensions).
+    const int g = t / TPH, dv0 = (t % TPH) * OPT;
+    if (g >= G) return;
+    float o[OPT];
 #pragma unroll
-  for (int g = 0; g < kMaxG; ++g) o[g] = 0.f;
-#pragma unroll
-  for (int jb = 0; jb < KPG; jb += 8) {
-    float v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int jj = kg * KPG + jb + u;
-      v[u] = 0.f;
-      if (jj < jn) {
-        const int j = j0 + jj;
-        const int pg = bt[j / p.page];
-        if (pg >= 0 && pg < p.num_pages)
-          v[u] = bf2f(p.v_plane[((static_cast<int64_t>(pg) * p.page + j % p.page) * p.Hkv + kh) * D + dv]);
+    for (int e = 0; e < OPT; ++e) o[e] = 0.f;
+    for (int key = 0; key < jn; ++key) {
+      const float pw = sc[g][key];
+      const uint16_t* vr = &Vs[key * KROW + dv0];
+      if (OPT == 4) {
+        const u32x2 v = *reinterpret_cast<const u32x2*>(vr);
+        o[0] += pw * bflo(v.x);
+        o[1] += pw * bfhi(v.x);
+        o[2] += pw * bflo(v.y);
+        o[3] += pw * bfhi(v.y);
+      } else {
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(vr);
+        o[0] += pw * bflo(v);
+        o[OPT - 1] += pw * bfhi(v);
       }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int jj = kg * KPG + jb + u;
-#pragma unroll
-      for (int g = 0; g < kMaxG; ++g)
-        if (g < G) o[g] += sc[g][jj] * v[u];
-    }
-  }
-#pragma unroll
-  for (int g = 0; g < kMaxG; ++g)
-    if (g < G) oacc[kg][g][dv] = o[g];
-  __syncthreads();
-  // partial record per (seq, head, split): [max, sum, o[0..D)]
-  for (int i = threadIdx.x; i < G * D; i += kDecThreads) {
-    const int g = i / D, e = i % D;
-    float t = 0.f;
-#pragma unroll
-    for (int q = 0; q < NG; ++q) t += oacc[q][g][e];
     float* rec = part + ((static_cast<int64_t>(s) * p.Hq + kh * G + g) * max_splits + split) * (D + 2);
-    rec[2 + e] = t;
-    if (e == 0) {
+#pragma unroll
+    for (int e = 0; e < OPT; ++e) rec[2 + dv0 + e] = o[e];
+    if (dv0 == 0) {
       rec[0] = stat[g][0];
       rec[1] = stat[g][1];
     }
@@ -456,38 +478,34 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnParams p, Ro
   const int n = rm.base_pos[s];
   const int nsplit = n / kDecSplit + 1;
   const float* base = part + (static_cast<int64_t>(s) * p.Hq + h) * max_splits * (D + 2);
-  // Online merge, eight split records per round so their loads overlap.
-  constexpr int U = 8;
-  float m = -INFINITY, l = 0.f, o = 0.f;
-  for (int k0 = 0; k0 < nsplit; k0 += U) {
-    float mk[U], lk[U], ok[U];
+  // Global max over the splits' maxima, then one weighted pass; records are
+  // read sixteen at a time so their loads overlap.
+  __shared__ float ms[kDecMaxSplitsLds];
+  __shared__ float ls[kDecMaxSplitsLds];
+  for (int k = threadIdx.x; k < nsplit; k += D) {
+    ms[k] = base[static_cast<int64_t>(k) * (D + 2)];
+    ls[k] = base[static_cast<int64_t>(k) * (D + 2) + 1];
+  }
+  __syncthreads();
+  float m = -INFINITY;
+  for (int k = 0; k < nsplit; ++k) m = fmaxf(m, ms[k]);
+  float l = 0.f, o = 0.f;
+  if (m != -INFINITY) {
+    constexpr int U = 16;
+    for (int k0 = 0; k0 < nsplit; k0 += U) {
+      float ok[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = k0 + u;
-      mk[u] = -INFINITY;
-      lk[u] = 0.f;
-      ok[u] = 0.f;
-      if (k < nsplit) {
-        const float* rec = base + static_cast<int64_t>(k) * (D + 2);
-        mk[u] = rec[0];
-        lk[u] = rec[1];
-        ok[u] = rec[2 + threadIdx.x];
+      for (int u = 0; u < U; ++u)
+        ok[u] = k0 + u < nsplit ? base[static_cast<int64_t>(k0 + u) * (D + 2) + 2 + threadIdx.x] : 0.f;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (k0 + u < nsplit) {
+          const float w = exp2f(ms[k0 + u] - m);   // a split with no valid key: max -inf, weight 0
+          l += w * ls[k0 + u];
+          o += w * ok[u];
+        }
       }
     }
-    float mg = m;
-#pragma unroll
-    for (int u = 0; u < U; ++u) mg = fmaxf(mg, mk[u]);
-    if (mg == -INFINITY) continue;
-    const float sc = exp2f(m - mg);   // m = -inf -> 0
-    l *= sc;
-    o *= sc;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float w = exp2f(mk[u] - mg);
-      l += w * lk[u];
-      o += w * ok[u];
-    }
-    m = mg;
   }
   p.o[(static_cast<int64_t>(rm.cu[s]) * p.Hq + h) * D + threadIdx.x] = f2bf(l > 0.f ? o / l : 0.f);
 }
@@ -527,7 +545,7 @@ hipError_t launch_attention_decode(const AttnParams& p, const RowMap& rm, float*
     nmax = std::max(nmax, rm.base_pos[i]);
   }
   const int splits = nmax / kDecSplit + 1;
-  if (splits > max_splits || p.Hq / p.Hkv > kMaxG) return hipErrorInvalidValue;
+  if (splits > max_splits || splits > kDecMaxSplitsLds || p.Hq / p.Hkv > kMaxG) return hipErrorInvalidValue;
   dim3 grid(splits, p.Hkv, rm.n_seqs);
   dim3 cgrid(p.Hq, rm.n_seqs);
   if (p.d == 128) {
