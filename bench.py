@@ -35,6 +35,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+NOMINAL_SCLK_GHZ = 2.4      # clock the MFMA peak is quoted at
 
 # Memory-side traffic of one gate|up GEMM launch at the large workload, from
 # two rocprofv3 --pmc passes over `bench.py --steps 1 --warmup 0
@@ -345,6 +346,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     roof_ms, roof_n = P.pallas_profile_read()["gemm_gate_up"]
+    roof_ghz, roof_wgs = P.pallas_profile_clock("gemm_gate_up")
     assert int(st.err.item()) == 0, "device-side error flag raised"
     # The same number of steps again with events around every launch:
     # per-class averages for the breakdown.
@@ -358,6 +360,7 @@ def main():
     p_end.record(stream)
     torch.cuda.synchronize()
     prof = P.pallas_profile_read()
+    gemm_sclk = {k: P.pallas_profile_clock(k)[0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")}
     ms_step_profiled = p_start.elapsed_time(p_end) / args.steps
     P.pallas_profile_enable([])
     assert int(st.err.item()) == 0, "device-side error flag raised"
@@ -375,6 +378,9 @@ def main():
     achieved = gu_flops / gu_avg_s / 1e12
     kernels = {k: {"avg_us": v[0] / v[1] * 1e3, "launches_per_step": v[1] / args.steps}
                for k, v in prof.items() if v[1]}
+    for k, ghz in gemm_sclk.items():
+        if k in kernels and ghz > 0:
+            kernels[k]["sclk_ghz"] = ghz
 
     out = {
         "metric": METRIC,
@@ -422,6 +428,11 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
+            # Shader clock measured inside the same launches (per-workgroup
+            # clock and wall-clock counters); the peak assumes 2.4 GHz.
+            "sclk_ghz": roof_ghz,
+            "frac_clock_adjusted": (achieved / (PEAK_BF16_TFLOPS * roof_ghz / NOMINAL_SCLK_GHZ)
+                                    if roof_ghz > 0 else None),
             "traffic": gemm_traffic_bytes(),
             "algorithmic_bytes": 2.0 * (prefix_tokens * cfg.hidden + 2 * cfg.ffn * cfg.hidden
                                         + prefix_tokens * cfg.ffn),

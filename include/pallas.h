@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define PALLAS_ABI_VERSION 1
+#define PALLAS_ABI_VERSION 2
 #define PALLAS_MAX_SEQS 64 /* sequences per prefill or decode call */
 #define PALLAS_MAX_PREFILL_LEN 32768 /* tokens per sequence in one prefill call */
 
@@ -265,6 +265,17 @@ int pallas_profile_read(double* ms, int64_t* launches);
 
 /* Zero the class totals and drop pending event pairs. */
 void pallas_profile_reset(void);
+
+/* Mean shader clock inside the timed launches of one kernel class since the
+ * last reset, in GHz (*mean_ghz; 0 when nothing was sampled), and the
+ * number of workgroups sampled (*workgroups, nullable).  Each workgroup of
+ * a sampled launch reads the shader-clock and constant-rate wall-clock
+ * counters at its start and end; the ratio of the sums, scaled by the
+ * wall-clock rate, is the clock the kernel actually ran at.  Sampled
+ * classes: the prefill GEMMs.  Synchronizes the device.  INVALID_ARG for a
+ * class outside [0, PALLAS_K_COUNT) or a null mean_ghz; HIP on a failed
+ * copy. */
+int pallas_profile_clock(int32_t kernel_class, double* mean_ghz, int64_t* workgroups);
 
 #ifdef __cplusplus
 }

@@ -12,5 +12,5 @@ from .binding import (  # noqa: F401
     pallas_model_create, pallas_model_destroy, pallas_workspace_size,
     pallas_prefill_prefix, pallas_pack_suffix_blocks, pallas_assemble_kv,
     pallas_decode_step, Model, ChunkDesc, ChunkHeader, EXPORTS, KERNEL_CLASSES,
-    pallas_profile_enable, pallas_profile_read, pallas_profile_reset,
+    pallas_profile_enable, pallas_profile_read, pallas_profile_reset, pallas_profile_clock,
 )

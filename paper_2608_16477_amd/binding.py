@@ -91,6 +91,7 @@ EXPORTS = {
     "pallas_profile_enable": (None, [C.c_uint32]),
     "pallas_profile_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     "pallas_profile_reset": (None, []),
+    "pallas_profile_clock": (C.c_int, [_i32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
 }
 
 KERNEL_CLASSES = ("embed", "rmsnorm", "rope_table", "gemm_qkv", "qkv_epilogue", "attention",
@@ -236,6 +237,15 @@ def pallas_profile_enable(classes=KERNEL_CLASSES):
 
 def pallas_profile_reset():
     lib().pallas_profile_reset()
+
+
+def pallas_profile_clock(kernel_class: str):
+    """(mean shader clock in GHz, workgroups sampled) inside the timed
+    launches of one kernel class since the last reset."""
+    ghz = C.c_double()
+    wgs = C.c_int64()
+    _check(lib().pallas_profile_clock(KERNEL_CLASSES.index(kernel_class), C.byref(ghz), C.byref(wgs)))
+    return ghz.value, wgs.value
 
 
 def pallas_profile_read():

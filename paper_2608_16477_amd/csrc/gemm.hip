@@ -67,6 +67,11 @@ __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint3
 
 template <int EPI>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
+  unsigned long long c0 = 0, w0 = 0;
+  if (p.clk) {
+    c0 = clock64();
+    w0 = wall_clock64();
+  }
   __shared__ __attribute__((aligned(16))) u32x4 lds[kStages][2][kSlots];  // [stage][A|B][slot]
 
   const int bid = blockIdx.x;
@@ -262,12 +267,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
       }
     }
   }
+  if (p.clk && threadIdx.x == 0) {
+    const unsigned long long c1 = clock64(), w1 = wall_clock64();
+    atomicAdd(&p.clk[0], c1 - c0);
+    atomicAdd(&p.clk[1], w1 - w0);
+    atomicAdd(&p.clk[2], 1ull);
+  }
 }
 
 }  // namespace
 
 hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
-                       int ldc, int M, int N, int K, hipStream_t s) {
+                       int ldc, int M, int N, int K, hipStream_t s, unsigned long long* clk) {
   const int64_t brows64 = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
   // byte offsets are 32-bit (buffer addressing): both operands below 2 GiB
   if (int64_t(M) * lda * 2 >= (int64_t(1) << 31) || brows64 * ldb * 2 >= (int64_t(1) << 31) ||
@@ -291,6 +302,7 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   p.a_bytes = static_cast<uint32_t>(int64_t(M) * lda * 2);
   const int64_t brows = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
   p.b_bytes = static_cast<uint32_t>(brows * ldb * 2);
+  p.clk = clk;
   const int grid = p.tiles_per_xcd * kXcds;
   switch (epi) {
     case kEpiBf16: gemm_bf16_kernel<kEpiBf16><<<grid, kThreads, 0, s>>>(p); break;

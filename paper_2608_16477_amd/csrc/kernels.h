@@ -55,12 +55,16 @@ struct GemmParams {
   int lda, ldb, ldc;
   int tiles_m, tiles_n, total_tiles, tiles_per_xcd, group_m;
   uint32_t a_bytes, b_bytes;
+  // Clock sampling (profiling only, else null): each workgroup adds its
+  // shader-clock cycles, wall-clock ticks and 1 to clk[0], clk[1], clk[2].
+  unsigned long long* clk;
 };
 
 // A bf16 [M][lda] (K columns used), B bf16 [rows][ldb]; K a multiple of 8;
 // A and B 16-byte aligned; M*lda*2 and rows*ldb*2 below 4 GiB.
 hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
-                       int ldc, int M, int N, int K, hipStream_t s);
+                       int ldc, int M, int N, int K, hipStream_t s,
+                       unsigned long long* clk = nullptr);
 
 }  // namespace pallas
 

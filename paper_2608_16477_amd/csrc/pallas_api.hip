@@ -388,7 +388,8 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
       PALLAS_TRY(PALLAS_K_QKV_EPI, pallas::launch_qkv_rope(qp, rm, M, s), "kv epilogue");
       break;
     }
-    PALLAS_TRY(PALLAS_K_GEMM_QKV, pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, M, QKV, H, s), "qkv gemm");
+    PALLAS_TRY(PALLAS_K_GEMM_QKV, pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, M, QKV, H, s,
+                                                      pallas::profile_clock_slot(PALLAS_K_GEMM_QKV)), "qkv gemm");
     qp.qkv = qkv;
     qp.qkv_ld = QKV;
     qp.kv_only = 0;
@@ -396,11 +397,14 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
     PALLAS_TRY(PALLAS_K_ATTN, pallas::launch_attention_prefill(ap, rm, s), "attention");
-    PALLAS_TRY(PALLAS_K_GEMM_O, pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, s), "o gemm");
+    PALLAS_TRY(PALLAS_K_GEMM_O, pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, s,
+                                                     pallas::profile_clock_slot(PALLAS_K_GEMM_O)), "o gemm");
     PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, M, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(PALLAS_K_GEMM_GATE_UP, pallas::launch_gemm(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, M, F, H, s),
+    PALLAS_TRY(PALLAS_K_GEMM_GATE_UP, pallas::launch_gemm(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, M, F, H, s,
+                                                         pallas::profile_clock_slot(PALLAS_K_GEMM_GATE_UP)),
                "gate_up gemm");
-    PALLAS_TRY(PALLAS_K_GEMM_DOWN, pallas::launch_gemm(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, M, H, F, s), "down gemm");
+    PALLAS_TRY(PALLAS_K_GEMM_DOWN, pallas::launch_gemm(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, M, H, F, s,
+                                                        pallas::profile_clock_slot(PALLAS_K_GEMM_DOWN)), "down gemm");
   }
   return PALLAS_OK;
 }

@@ -10,6 +10,9 @@ namespace pallas {
 bool profile_on(int cls);
 void profile_record(int cls, hipEvent_t begin, hipEvent_t end);
 hipEvent_t profile_event();
+// Device counters [cycles, wall ticks, workgroups] for clock sampling inside
+// the launches of `cls`, or null when the class is not being timed.
+unsigned long long* profile_clock_slot(int cls);
 
 // Brackets the launches issued during its lifetime on `s`.
 class ProfScope {

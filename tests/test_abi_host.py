@@ -34,7 +34,7 @@ def test_exports_every_declared_call(P):
     for n in names:
         assert hasattr(h, n), n
     assert set(names) == set(P.EXPORTS), "binding and header disagree"
-    assert P.pallas_abi_version() == 1
+    assert P.pallas_abi_version() == 2
 
 
 @pytest.mark.parametrize("prefix,ranges,n,ok", top.test_check_coverage.pytestmark[0].args[1])
@@ -160,3 +160,15 @@ def test_prefill_rejects_sequences_beyond_the_length_limit(P):
         assert rc(limit) == P.Status.WORKSPACE
     finally:
         h.pallas_model_destroy(model)
+
+
+def test_profile_clock_arguments(P):
+    """The clock query rejects a class outside the enumeration; with nothing
+    sampled it reports 0 GHz and 0 workgroups."""
+    h = P.lib()
+    ghz, wgs = C.c_double(7.0), C.c_int64(7)
+    assert h.pallas_profile_clock(13, C.byref(ghz), C.byref(wgs)) == P.Status.INVALID_ARG
+    assert h.pallas_profile_clock(-1, C.byref(ghz), C.byref(wgs)) == P.Status.INVALID_ARG
+    assert h.pallas_profile_clock(7, None, C.byref(wgs)) == P.Status.INVALID_ARG
+    assert h.pallas_profile_clock(7, C.byref(ghz), C.byref(wgs)) == P.Status.OK
+    assert ghz.value == 0.0 and wgs.value == 0
