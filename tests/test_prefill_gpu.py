@@ -114,3 +114,27 @@ def test_causality_and_determinism(P):
     b = kv_logical(pre, bt, p)
     np.testing.assert_array_equal(a, b)
     assert torch.equal(pre.view(torch.int16), pre2.view(torch.int16))
+
+
+def test_profile_clock_samples_gemm_launches(P):
+    """With timing on for the gate|up GEMM, a prefill records every one of
+    its workgroups and a shader clock between 0.3 and 3.5 GHz; with timing
+    off nothing is sampled."""
+    cfg = configs.TINY
+    glob, layers = gen.model_weights(cfg, seed=6)
+    model = gpu_model(P, cfg, glob, layers)
+    ids = gen.token_ids(300, cfg.vocab, seed=6).numpy()
+    bt = gen.block_table(19, 24, 19, 6, 1)
+    P.pallas_profile_reset()
+    run_prefill(P, model, cfg, [ids], [bt], 24)
+    assert P.pallas_profile_clock("gemm_gate_up") == (0.0, 0)
+    P.pallas_profile_enable(["gemm_gate_up"])
+    try:
+        run_prefill(P, model, cfg, [ids], [bt], 24)
+        ghz, wgs = P.pallas_profile_clock("gemm_gate_up")
+    finally:
+        P.pallas_profile_enable([])
+        P.pallas_profile_reset()
+    tiles = -(-300 // 256) * -(-cfg.ffn // 128)        # M tiles x (gate|up column groups of 128)
+    assert wgs == tiles * (cfg.n_layers - 1)
+    assert 0.3 < ghz < 3.5
