@@ -1,13 +1,13 @@
 // Skinny GEMM for decode (M <= 8 rows): C = X W^T streaming the weights once.
 //
-// A workgroup of 8 waves owns one 16-row weight tile (two for the gate|up
-// projection: 16 gate rows and the matching 16 up rows) and splits K eight
+// A workgroup of 4 waves owns one 16-row weight tile (two for the gate|up
+// projection: 16 gate rows and the matching 16 up rows) and splits K four
 // ways.  Each wave streams its K range in steps of 64: one 128-byte line of
 // each weight row and the matching 64 columns of X go straight from memory
 // into a private LDS stage with buffer_load ... lds (three stages in
 // flight), each load instruction covering whole lines of 8 rows.  Inside a
 // stage the 16-byte slots are permuted so the v_mfma_f32_16x16x32_bf16
-// operand reads (16 rows at one k) hit 16 distinct bank groups.  The eight
+// operand reads (16 rows at one k) hit 16 distinct bank groups.  The four
 // partial tiles are summed through LDS and the epilogue matches the prefill
 // GEMM's.
 #include "common.h"
@@ -17,7 +17,7 @@ namespace pallas {
 
 namespace {
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kStages = 3;
 constexpr int kKStep = 64;        // k per stage: one 128-byte line per weight row
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
     compute(s);
   }
 
-  // Sum the eight partial tiles.
+  // Sum the per-wave partial tiles.
   __syncthreads();
   f32x4* red = reinterpret_cast<f32x4*>(lds);
 #pragma unroll
