@@ -6,8 +6,11 @@
 // so one wave's barrier and LDS waits overlap the other's MFMAs), each wave
 // 128 x 64 as 4 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at
 // a time through a double-buffered LDS stage (2 x (32 KiB A + 32 KiB B))
-// filled by buffer loads that write LDS directly (no register staging),
-// issued one K-step ahead; one barrier per step.  64-element K-steps make
+// filled by buffer loads that write LDS directly (no register staging);
+// one barrier per step.  Step kt+2's loads are issued right after the
+// barrier inside step kt that releases kt's slot, so they have a whole
+// K-step to land (issued at the top of step kt+1 they had three quarters of
+// one, and the loop waited on them).  64-element K-steps make
 // every operand row segment a whole 128-byte line, so each L1 miss request
 // carries 128 bytes: the kernel is bound by how many misses a CU keeps in
 // flight against L2 latency, and full-line requests double the bytes per
@@ -135,20 +138,21 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     brow[j] = (EPI == kEpiSwiGLU ? j * 128 + wn * 32 : wn * 64 + j * 32) + l32;
 
   const int KT = (p.K + BK - 1) / BK;
-  // Prologue: stages 0 .. kStages-2 in flight; then stage 0 resident.
-#pragma unroll
-  for (int st = 0; st < kStages - 1; ++st) {
-    if (st < KT && wave < kLoaderWaves) {
-      load_tile_lds(ra, p.a_bytes, a_off, chunk, st * BK, p.K, lds[st][0], wave, lane);
-      load_tile_lds(rb, p.b_bytes, b_off, chunk, st * BK, p.K, lds[st][1], wave, lane);
+  // Prologue: steps 0 and 1 in flight; then step 0 resident.
+  if (wave < kLoaderWaves) {
+    load_tile_lds(ra, p.a_bytes, a_off, chunk, 0, p.K, lds[0][0], wave, lane);
+    load_tile_lds(rb, p.b_bytes, b_off, chunk, 0, p.K, lds[0][1], wave, lane);
+    if (KT > 1) {
+      load_tile_lds(ra, p.a_bytes, a_off, chunk, BK, p.K, lds[1][0], wave, lane);
+      load_tile_lds(rb, p.b_bytes, b_off, chunk, BK, p.K, lds[1][1], wave, lane);
     }
   }
-  if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads * (kStages - 2)) : "memory");
+  if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads) : "memory");
   else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
 
-  // Fragment registers: [k-half][block]; half 0 of step kt is read during
-  // step kt-1, half 1 during the first half of step kt.
+  // Fragment registers: [substep parity][block]; substep 0 of step kt is
+  // read during the last substep of step kt-1.
   bf16x8 fa[2][4], fb[2][2];
   auto read_frags = [&](int slot, int kk, bf16x8* a, bf16x8* b) {
     const u32x4* At = lds[slot][0];
@@ -166,65 +170,61 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
       for (int j = 0; j < 2; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   };
+  // One LDS read between consecutive MFMAs of a substep ...
+  auto sched_reads = [] {
+#pragma unroll
+    for (int q = 0; q < 6; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+    }
+  };
+  // ... and, in a loader wave's refill substep, two of its 16 loads as well.
+  auto sched_reads_loads = [] {
+#pragma unroll
+    for (int q = 0; q < 6; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // 2 global loads
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+  };
   read_frags(0, 0, fa[0], fb[0]);
 
-  // One K-step: refill the slot of step kt-1 (kRefill); MFMAs on substep kk
-  // while substep kk+1 is read; before the last substep, wait for stage
-  // kt+1 and barrier; the last substep's MFMAs then overlap the reads of
-  // step kt+1's first substep.  The steady loop has no branches so the LDS
-  // reads interleave with the MFMAs.
+  // One K-step: MFMAs on substep kk while substep kk+1 is read from slot
+  // kt%2; before the last substep, wait for step kt+1 and barrier.  After
+  // that barrier no wave reads slot kt%2 again, so step kt+2's loads
+  // (kRefill) go there at once, between the last substep's MFMAs, which
+  // also overlap the reads of step kt+1's first substep.  The steady loop
+  // has no branches so the LDS reads interleave with the MFMAs.
   auto step = [&](int kt, auto refill_tag, auto loader_tag) {
     constexpr bool kRefill = decltype(refill_tag)::value;
     constexpr bool kLoader = decltype(loader_tag)::value;
-    const int slot = kt % kStages;
-    if (kRefill && kLoader) {
-      const int nk = kt + kStages - 1;
-      const int ns = nk % kStages;
-      load_tile_lds(ra, p.a_bytes, a_off, chunk, nk * BK, p.K, lds[ns][0], wave, lane);
-      load_tile_lds(rb, p.b_bytes, b_off, chunk, nk * BK, p.K, lds[ns][1], wave, lane);
-    }
+    const int slot = kt & 1;
 #pragma unroll
     for (int kk = 0; kk < KK - 1; ++kk) {
       read_frags(slot, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
       mfma_block(fa[kk & 1], fb[kk & 1]);
-      if (kRefill && kLoader && kk == 0) {
-        // all refill loads ride between this substep's MFMAs
-#pragma unroll
-        for (int q = 0; q < 6; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-          __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // 2 global loads
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
-      } else {
-#pragma unroll
-        for (int q = 0; q < 6; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-        }
-      }
+      sched_reads();
     }
-    if (kRefill)
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads * (kStages - 2)) : "memory");
-    else
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
+    if (kRefill && kLoader) {
+      load_tile_lds(ra, p.a_bytes, a_off, chunk, (kt + 2) * BK, p.K, lds[slot][0], wave, lane);
+      load_tile_lds(rb, p.b_bytes, b_off, chunk, (kt + 2) * BK, p.K, lds[slot][1], wave, lane);
+    }
     // Step kt+1 is resident; its slot index is valid even past the end
     // (the fragments are then unused).
-    read_frags((kt + 1) % kStages, 0, fa[KK & 1], fb[KK & 1]);
+    read_frags(slot ^ 1, 0, fa[KK & 1], fb[KK & 1]);
     mfma_block(fa[(KK - 1) & 1], fb[(KK - 1) & 1]);
-#pragma unroll
-    for (int q = 0; q < 6; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
+    if (kRefill && kLoader) sched_reads_loads();
+    else sched_reads();
   };
   // The K-loop is specialised per role so the loader waves' loads sit in
   // the same scheduling region as their MFMAs.
   auto main_loop = [&](auto loader_tag) {
     int kt = 0;
-    for (; kt + kStages - 1 < KT; ++kt) step(kt, std::true_type{}, loader_tag);
+    for (; kt + 2 < KT; ++kt) step(kt, std::true_type{}, loader_tag);
     for (; kt < KT; ++kt) step(kt, std::false_type{}, loader_tag);
   };
   if (wave < kLoaderWaves) main_loop(std::true_type{});
