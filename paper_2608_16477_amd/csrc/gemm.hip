@@ -232,6 +232,52 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
 
   // Epilogue.  Accumulator register r of block (i, j) holds
   // row wm*128 + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.
+  if (EPI == kEpiAddF32) {
+    // Residual add through buffer accesses on this tile's rows: out-of-range
+    // rows and columns get an offset past the range, so loads read 0 and
+    // stores are dropped without a branch.  Written as C[i] += acc, a load
+    // could not pass the previous store (they may alias) and each element
+    // paid a memory round trip; here the 32 residual values of row block
+    // i+1 are loaded before the sums of block i are stored.
+    // (readfirstlane keeps the descriptor in scalar registers; computed in
+    // vector registers it would need a loop around every access)
+    const int m0s = __builtin_amdgcn_readfirstlane(m0);
+    const uint32_t c_bytes = static_cast<uint32_t>(min(p.M - m0s, BM)) * p.ldc * 4u;
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        static_cast<float*>(p.C) + static_cast<int64_t>(m0s) * p.ldc, 0, c_bytes, 0x00020000);
+    auto off = [&](int i, int r, int j) -> uint32_t {
+      const int row = wm * 128 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+      const int col = tn * BN + wn * 64 + j * 32 + l32;
+      return col < p.N ? static_cast<uint32_t>(row * p.ldc + col) * 4u : c_bytes;
+    };
+    float cv[2][2][16];  // [buffer][j][r]
+    auto load_block = [&](int i, float (*v)[16]) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          v[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, off(i, r, j), 0, 0));
+    };
+    load_block(0, cv[0]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (i + 1 < 4) load_block(i + 1, cv[(i + 1) & 1]);
+      // The sums go back into the accumulators and are stored from there:
+      // a store reads its data register late, so storing from cv would make
+      // the loads of block i+2 wait for these stores.  (The sum goes through
+      // a temporary: writing acc[i][j][r] and reading it back in the same
+      // unrolled loop was miscompiled by the ROCm 7.2 clang; a probe stored
+      // element 0's sum for every r.)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const float sum = cv[i & 1][j][r] + acc[i][j][r];
+          acc[i][j][r] = sum;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sum), rc, off(i, r, j), 0, 0);
+        }
+    }
+  } else {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -253,10 +299,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
         for (int j = 0; j < 2; ++j) {
           const int col = tn * BN + wn * 64 + j * 32 + l32;
           if (col >= p.N) continue;
-          if (EPI == kEpiAddF32) {
-            float* C = static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc;
-            C[col] += acc[i][j][r];
-          } else if (EPI == kEpiF32) {
+          if (EPI == kEpiF32) {
             float* C = static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc;
             C[col] = acc[i][j][r];
           } else {
@@ -266,6 +309,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
         }
       }
     }
+  }
   }
   if (p.clk && threadIdx.x == 0) {
     const unsigned long long c1 = clock64(), w1 = wall_clock64();
