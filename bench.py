@@ -74,6 +74,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stress", action="store_true",
                     help="skip the stress-layout copy measurements (suffixes of 64-4096 tokens)")
+    ap.add_argument("--no-chunked", action="store_true",
+                    help="skip the chunked-prefill measurements (256-token chunks, with 0-3 "
+                         "resident decode sessions interleaved)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device-to-device copy and exit (the reference "
                          "point for scaling FETCH_SIZE / WRITE_SIZE counter readings)")
@@ -245,6 +248,76 @@ def copies_stress(P, seed):
     return {"layout": (f"{L} layers, {hkv} KV heads, head_dim {d}: {n_src}-token source in "
                        f"{src_pages} shuffled pages; {tp}-page target, half occupied; "
                        f"{c}-token chunks"), "rows": rows, "per_chunk_launch": lat}
+
+
+def chunked_prefill(st, chunk=256, residents=(0, 1, 2, 3), reps=3, resident_ctx=2000):
+    """The workload's first prefix prefilled in `chunk`-token chunks
+    (pallas_prefill_chunk), each chunk attending to the earlier chunks
+    through the target pool; then the same with R resident sessions
+    interleaved, one batched decode step of the R residents after every
+    chunk (the concurrency experiment's contention with resident
+    decoding).  The residents decode over their own `resident_ctx`-token
+    caches in a separate pool (N(0,1) bf16 K/V).  Median of `reps` runs
+    after one warm-up; the whole prefix's time, migration tokens/s, and the
+    residents' mean decode-step time."""
+    import numpy as np
+    import torch
+    from workloads import gen
+
+    P, cfg, model = st.P, st.cfg, st.model
+    p = st.ps[0]
+    ids = torch.tensor(st.ids[0][:p], dtype=torch.int32, device="cuda")
+    bt = st.dst_tab[:1]
+    bounds = [(a, min(a + chunk, p)) for a in range(0, p, chunk)]
+    ws = model.workspace(chunk, max(1, max(residents)))
+    err = st.err
+    rmax = max(residents)
+    if rmax:
+        rpages = (resident_ctx + 1 + 15) // 16
+        rpool = gen.kv_pool_normal(cfg.n_layers, rmax * rpages, cfg.page_size, cfg.n_kv_heads,
+                                   cfg.head_dim, seed=11, device="cuda")
+        rtab = torch.arange(rmax * rpages, dtype=torch.int32, device="cuda").view(rmax, rpages)
+        rtok = torch.randint(0, cfg.vocab, (rmax,), dtype=torch.int32, device="cuda")
+        rlog = torch.empty((rmax, cfg.vocab), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def run(R, evs=None):
+        for k, (a, b) in enumerate(bounds):
+            model.prefill_chunk(ids[a:b], [0, b - a], [a], bt, st.dst, ws, err)
+            if R:
+                if evs is not None:
+                    evs[k][0].record(stream)
+                model.decode_step(rtok[:R], [resident_ctx] * R, rtab[:R], rpool, rlog[:R], ws, err)
+                if evs is not None:
+                    evs[k][1].record(stream)
+
+    flops = cfg.prefill_flops(p)
+    out = {"chunk_tokens": chunk, "prefix_tokens": p, "chunks": len(bounds), "rows": []}
+    for R in residents:
+        run(R)
+        times, itl = [], []
+        for _ in range(reps):
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in bounds]
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            run(R, evs)
+            b.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+            if R:
+                itl.append(float(np.mean([x.elapsed_time(y) for x, y in evs])))
+        ms = float(np.median(times))
+        row = {"residents": R, "ms": ms, "migration_tokens_per_s": p / ms * 1e3}
+        if R == 0:
+            row["tflops"] = flops / ms / 1e9
+            row["mfma_frac"] = flops / ms / 1e9 / PEAK_BF16_TFLOPS
+        else:
+            row["resident_decode_step_ms"] = float(np.median(itl))
+        out["rows"].append(row)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0, "device-side error flag raised in the chunked prefill"
+    return out
 
 
 def cpu_baseline(setup):
@@ -439,6 +512,10 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if not args.no_chunked:
+        print("[bench] chunked prefill", file=sys.stderr, flush=True)
+        out["chunked_prefill"] = chunked_prefill(st)
+        out["chunked_prefill"]["whole_prefix_ms"] = phase_ms["prefill"]
     if not args.no_stress:
         print("[bench] stress-layout copies", file=sys.stderr, flush=True)
         out["copies_stress"] = copies_stress(P, args.seed)

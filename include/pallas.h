@@ -13,6 +13,7 @@
  *
  * Calls:
  *   pallas_prefill_prefix      prefix prefill writing K/V into paged blocks
+ *   pallas_prefill_chunk       the same, one chunk at a time over earlier chunks
  *   pallas_pack_suffix_blocks  gather suffix pages into transfer chunks
  *   pallas_assemble_kv         scatter chunks into the target block table
  *   pallas_decode_step         one decode step over an assembled cache
@@ -44,7 +45,7 @@
 extern "C" {
 #endif
 
-#define PALLAS_ABI_VERSION 2
+#define PALLAS_ABI_VERSION 3
 #define PALLAS_MAX_SEQS 64 /* sequences per prefill or decode call */
 #define PALLAS_MAX_PREFILL_LEN 32768 /* tokens per sequence in one prefill call */
 
@@ -177,6 +178,28 @@ int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_to
                           const int32_t* h_cu_seqlens, const int32_t* d_block_tables,
                           int32_t max_pages, const pallas_kv_pool* pool, void* d_workspace,
                           size_t ws_bytes, int32_t* d_err, void* stream);
+
+/* Chunked prefill (Section 4.5, contention with resident decoding: the
+ * target interleaves prefix reconstruction with decode steps by prefilling
+ * in chunks; the concurrency evaluation, Section 6.4, uses 256-token
+ * chunks).
+ *
+ * As pallas_prefill_prefix, except that the ids of sequence i sit at
+ * positions s_i .. s_i + p_i - 1 with s_i = h_start_pos[i] (host, >= 0), and
+ * each of them attends to the K/V of positions [0, s_i) already in the pool
+ * through the same block-table row (written by earlier calls, e.g. the
+ * previous chunks) as well as to the chunk's own earlier positions.  Only
+ * slots [s_i, s_i + p_i) are written.  A prefix prefilled chunk by chunk
+ * gives the same cache, up to rounding, as one prefill over the whole
+ * prefix.  Limits: s_i + p_i <= max_pages * page (OUT_OF_RANGE) and
+ * <= PALLAS_MAX_PREFILL_LEN (UNSUPPORTED); sum p_i <= the workspace's
+ * max_tokens.  Slots [0, s_i) are read, never checked: the caller must
+ * have filled them. */
+int pallas_prefill_chunk(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
+                         const int32_t* h_cu_seqlens, const int32_t* h_start_pos,
+                         const int32_t* d_block_tables, int32_t max_pages,
+                         const pallas_kv_pool* pool, void* d_workspace, size_t ws_bytes,
+                         int32_t* d_err, void* stream);
 
 /* Suffix-block extraction (Section 4.3, Section 5: per-layer K/V of
  * completed blocks, taken by physical block id from the GPU cache).

@@ -216,6 +216,30 @@ def prefill(ids: Sequence[int], glob: Dict, layers: List[Dict], shp: Shape,
     return K, V, r
 
 
+def prefill_chunk(ids: Sequence[int], start: int, K_cache: List[np.ndarray],
+                  V_cache: List[np.ndarray], glob: Dict, layers: List[Dict], shp: Shape,
+                  rnd: Rounder = bf16_round, n_layers: Optional[int] = None):
+    """Chunked prefill (Section 4.5: the target interleaves prefix
+    reconstruction with resident decoding by prefilling in chunks).
+
+    The tokens ``ids`` sit at positions ``start .. start + T - 1``; each one
+    attends causally to the cached positions ``0 .. start - 1``
+    (``K_cache[l], V_cache[l]`` hold at least ``[start, Hkv, d]``) and to
+    the chunk's tokens up to itself.  Returns per-layer ``[T, Hkv, d]`` K and
+    V of the chunk (the last evaluated layer stops once they exist)."""
+    L = shp.n_layers if n_layers is None else n_layers
+    pos = start + np.arange(len(ids))
+    r = embed(ids, glob)
+    K, V = [], []
+    for l in range(L):
+        kp = K_cache[l][:start] if start > 0 else None
+        vp = V_cache[l][:start] if start > 0 else None
+        r, k, v = layer(r, pos, kp, vp, layers[l], shp, rnd, kv_only=(l == L - 1))
+        K.append(k)
+        V.append(v)
+    return K, V
+
+
 def decode(token: int, n: int, K_cache: List[np.ndarray], V_cache: List[np.ndarray],
            glob: Dict, layers: List[Dict], shp: Shape, rnd: Rounder = bf16_round):
     """One decode step: token ``token`` at position ``n`` attends to the

@@ -10,7 +10,7 @@ from .binding import (  # noqa: F401
     PallasError, Status, lib, library_path,
     pallas_abi_version, pallas_last_error, pallas_check_coverage,
     pallas_model_create, pallas_model_destroy, pallas_workspace_size,
-    pallas_prefill_prefix, pallas_pack_suffix_blocks, pallas_assemble_kv,
+    pallas_prefill_prefix, pallas_prefill_chunk, pallas_pack_suffix_blocks, pallas_assemble_kv,
     pallas_decode_step, Model, ChunkDesc, ChunkHeader, EXPORTS, KERNEL_CLASSES,
     pallas_profile_enable, pallas_profile_read, pallas_profile_reset, pallas_profile_clock,
 )

@@ -81,6 +81,8 @@ EXPORTS = {
     "pallas_workspace_size": (_sz, [_vp, _i32, _i32]),
     "pallas_prefill_prefix": (C.c_int, [_vp, _i32, _vp, _pi32, _vp, _i32, C.POINTER(KVPoolC),
                                         _vp, _sz, _vp, _vp]),
+    "pallas_prefill_chunk": (C.c_int, [_vp, _i32, _vp, _pi32, _pi32, _vp, _i32, C.POINTER(KVPoolC),
+                                       _vp, _sz, _vp, _vp]),
     "pallas_pack_suffix_blocks": (C.c_int, [C.POINTER(KVPoolC), _vp, _i32, C.POINTER(ChunkDesc),
                                             _i32, _vp, _sz, _vp, _vp]),
     "pallas_assemble_kv": (C.c_int, [C.POINTER(KVPoolC), _vp, _i32, C.POINTER(ChunkHeader), _vp,
@@ -217,6 +219,17 @@ def pallas_prefill_prefix(h, token_ids, cu_seqlens: Sequence[int], block_tables,
                                        _stream(stream)))
 
 
+def pallas_prefill_chunk(h, token_ids, cu_seqlens: Sequence[int], start_pos: Sequence[int],
+                         block_tables, pool, workspace, err=None, stream=None):
+    assert len(start_pos) == len(cu_seqlens) - 1
+    ps = kv_pool_struct(pool)
+    _check(lib().pallas_prefill_chunk(h, len(cu_seqlens) - 1, _ptr(token_ids),
+                                      _i32_array(cu_seqlens), _i32_array(start_pos),
+                                      _ptr(block_tables), block_tables.shape[-1], C.byref(ps),
+                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _ptr(err), _stream(stream)))
+
+
 def pallas_decode_step(h, tokens, positions: Sequence[int], block_tables, pool, logits,
                        workspace, err=None, stream=None):
     ps = kv_pool_struct(pool)
@@ -287,6 +300,11 @@ class Model:
                        stream=None):
         pallas_prefill_prefix(self.handle, token_ids, cu_seqlens, block_tables, pool, workspace,
                               err, stream)
+
+    def prefill_chunk(self, token_ids, cu_seqlens, start_pos, block_tables, pool, workspace,
+                      err=None, stream=None):
+        pallas_prefill_chunk(self.handle, token_ids, cu_seqlens, start_pos, block_tables, pool,
+                             workspace, err, stream)
 
     def decode_step(self, tokens, positions, block_tables, pool, logits, workspace, err=None,
                     stream=None):

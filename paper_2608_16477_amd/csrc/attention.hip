@@ -71,16 +71,23 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
   const int gidx = sch.total - 1 - static_cast<int>(blockIdx.x);  // longest blocks first
   int s = 0;
   while (s + 1 < rm.n_seqs && sch.prefix[s + 1] <= gidx) ++s;
-  const int q0 = (gidx - sch.prefix[s]) * QB;
+  // Query blocks sit at absolute positions [32 b, 32 b + 32): the rows of
+  // sequence s are positions [base, base + len), so with base > 0 (a chunk
+  // over earlier chunks) the first block may be partly before the chunk.
+  // Aligned blocks keep every key tile but the last wholly visible to
+  // every query of the block, and give a query the same key tiles as an
+  // undivided prefill would.
+  const int base = rm.base_pos[s];
   const int len = rm.cu[s + 1] - rm.cu[s];
-  const int row0 = rm.cu[s];
+  const int q0 = ((base / QB) + (gidx - sch.prefix[s])) * QB;
+  const int row0 = rm.cu[s] - base;   // row of absolute position a: row0 + a
   const int32_t* bt = p.bt + static_cast<int64_t>(s) * p.max_pages;
 
   const int qpos = q0 + l32;
-  const bool qvalid = qpos < len;
+  const bool qvalid = qpos >= base && qpos < base + len;
   bf16x8 qf[D / 16];
   {
-    const uint16_t* qrow = p.q + (static_cast<int64_t>(row0 + (qvalid ? qpos : 0)) * p.Hq + h) * D;
+    const uint16_t* qrow = p.q + (static_cast<int64_t>(row0 + (qvalid ? qpos : base)) * p.Hq + h) * D;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       u32x4 v = qvalid ? *reinterpret_cast<const u32x4*>(qrow + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
@@ -88,7 +95,7 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
     }
   }
 
-  const int kend = min(q0 + QB, len);
+  const int kend = min(q0 + QB, base + len);
   const int ntiles = (kend + KB - 1) / KB;
   {
     // This sequence's block-table entries for keys [0, kend), read once.
@@ -286,7 +293,7 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = k0 + t * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-        if (key > qpos || key >= len) st[t][r] = -INFINITY;
+        if (key > qpos || key >= kend) st[t][r] = -INFINITY;
       }
     float alpha;
     if (softmax(st, alpha)) rescale(alpha);
@@ -517,9 +524,10 @@ hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipSt
   sch.prefix[0] = 0;
   int maxlen = 0;
   for (int i = 0; i < rm.n_seqs; ++i) {
-    const int len = rm.cu[i + 1] - rm.cu[i];
-    maxlen = std::max(maxlen, len);
-    sch.prefix[i + 1] = sch.prefix[i] + (len + QB - 1) / QB;
+    const int len = rm.cu[i + 1] - rm.cu[i], base = rm.base_pos[i];
+    if (len < 1 || base < 0) return hipErrorInvalidValue;
+    maxlen = std::max(maxlen, base + len);
+    sch.prefix[i + 1] = sch.prefix[i] + (base + len + QB - 1) / QB - base / QB;
   }
   sch.total = sch.prefix[rm.n_seqs];
   if (sch.total == 0) return hipSuccess;

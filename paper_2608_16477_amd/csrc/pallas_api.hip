@@ -488,37 +488,68 @@ size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t 
   return pallas::workspace_bytes(m->cfg, max_tokens, max_seqs);
 }
 
-int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
-                          const int32_t* h_cu_seqlens, const int32_t* d_block_tables,
-                          int32_t max_pages, const pallas_kv_pool* pool, void* d_workspace,
-                          size_t ws_bytes, int32_t* d_err, void* stream) {
-  if (!m) return fail(PALLAS_ERR_INVALID_ARG, "prefill: null model");
+}  // extern "C"
+
+namespace {
+
+// Shared by the whole-prefix and the chunked prefill: sequence i's ids sit
+// at positions start[i] .. start[i] + p_i - 1 (start null: all 0).
+int prefill_call(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
+                 const int32_t* h_cu_seqlens, const int32_t* h_start_pos,
+                 const int32_t* d_block_tables, int32_t max_pages, const pallas_kv_pool* pool,
+                 void* d_workspace, size_t ws_bytes, int32_t* d_err, void* stream,
+                 const char* what) {
+  if (!m) return fail(PALLAS_ERR_INVALID_ARG, "%s: null model", what);
   if (num_seqs < 1 || num_seqs > PALLAS_MAX_SEQS)
-    return fail(PALLAS_ERR_INVALID_ARG, "prefill: num_seqs %d outside [1, %d]", num_seqs, PALLAS_MAX_SEQS);
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: num_seqs %d outside [1, %d]", what, num_seqs, PALLAS_MAX_SEQS);
   if (!d_token_ids || !h_cu_seqlens || !d_block_tables || max_pages <= 0)
-    return fail(PALLAS_ERR_INVALID_ARG, "prefill: null ids, cu_seqlens or block tables");
-  if (int rc = check_model_pool(m, pool, "prefill")) return rc;
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: null ids, cu_seqlens or block tables", what);
+  if (int rc = check_model_pool(m, pool, what)) return rc;
   pallas::RowMap rm;
   rm.n_seqs = num_seqs;
-  if (h_cu_seqlens[0] != 0) return fail(PALLAS_ERR_INVALID_ARG, "prefill: cu_seqlens[0] must be 0");
+  if (h_cu_seqlens[0] != 0) return fail(PALLAS_ERR_INVALID_ARG, "%s: cu_seqlens[0] must be 0", what);
   const int64_t cap = int64_t(max_pages) * pool->page_size;
   for (int i = 0; i <= num_seqs; ++i) rm.cu[i] = h_cu_seqlens[i];
   for (int i = 0; i < num_seqs; ++i) {
     const int64_t len = int64_t(h_cu_seqlens[i + 1]) - h_cu_seqlens[i];
-    if (len < 1) return fail(PALLAS_ERR_INVALID_ARG, "prefill: sequence %d has length %lld", i, (long long)len);
-    if (len > cap)
-      return fail(PALLAS_ERR_OUT_OF_RANGE, "prefill: sequence %d of %lld tokens exceeds the table (%lld)", i,
-                  (long long)len, (long long)cap);
-    if (len > PALLAS_MAX_PREFILL_LEN)
-      return fail(PALLAS_ERR_UNSUPPORTED, "prefill: sequence %d of %lld tokens (at most %d per call)", i,
-                  (long long)len, PALLAS_MAX_PREFILL_LEN);
-    rm.base_pos[i] = 0;
+    const int64_t start = h_start_pos ? h_start_pos[i] : 0;
+    if (len < 1) return fail(PALLAS_ERR_INVALID_ARG, "%s: sequence %d has length %lld", what, i, (long long)len);
+    if (start < 0) return fail(PALLAS_ERR_INVALID_ARG, "%s: sequence %d starts at %lld", what, i, (long long)start);
+    if (start + len > cap)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "%s: sequence %d positions [%lld, %lld) exceed the table (%lld)", what,
+                  i, (long long)start, (long long)(start + len), (long long)cap);
+    if (start + len > PALLAS_MAX_PREFILL_LEN)
+      return fail(PALLAS_ERR_UNSUPPORTED, "%s: sequence %d reaches position %lld (at most %d)", what, i,
+                  (long long)(start + len), PALLAS_MAX_PREFILL_LEN);
+    rm.base_pos[i] = static_cast<int32_t>(start);
   }
   const int64_t M = h_cu_seqlens[num_seqs];
-  if (M > (int64_t(1) << 24)) return fail(PALLAS_ERR_UNSUPPORTED, "prefill: too many tokens");
-  if (int rc = check_workspace(m, d_workspace, ws_bytes, M, num_seqs, "prefill")) return rc;
+  if (M > (int64_t(1) << 24)) return fail(PALLAS_ERR_UNSUPPORTED, "%s: too many tokens", what);
+  if (int rc = check_workspace(m, d_workspace, ws_bytes, M, num_seqs, what)) return rc;
   return run_prefill(m, rm, static_cast<int>(M), d_token_ids, d_block_tables, max_pages, pool,
                      static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
+                          const int32_t* h_cu_seqlens, const int32_t* d_block_tables,
+                          int32_t max_pages, const pallas_kv_pool* pool, void* d_workspace,
+                          size_t ws_bytes, int32_t* d_err, void* stream) {
+  return prefill_call(m, num_seqs, d_token_ids, h_cu_seqlens, nullptr, d_block_tables, max_pages,
+                      pool, d_workspace, ws_bytes, d_err, stream, "prefill");
+}
+
+int pallas_prefill_chunk(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
+                         const int32_t* h_cu_seqlens, const int32_t* h_start_pos,
+                         const int32_t* d_block_tables, int32_t max_pages,
+                         const pallas_kv_pool* pool, void* d_workspace, size_t ws_bytes,
+                         int32_t* d_err, void* stream) {
+  if (!h_start_pos) return fail(PALLAS_ERR_INVALID_ARG, "prefill chunk: null start positions");
+  return prefill_call(m, num_seqs, d_token_ids, h_cu_seqlens, h_start_pos, d_block_tables, max_pages,
+                      pool, d_workspace, ws_bytes, d_err, stream, "prefill chunk");
 }
 
 int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_tokens,

@@ -34,7 +34,7 @@ def test_exports_every_declared_call(P):
     for n in names:
         assert hasattr(h, n), n
     assert set(names) == set(P.EXPORTS), "binding and header disagree"
-    assert P.pallas_abi_version() == 2
+    assert P.pallas_abi_version() == 3
 
 
 @pytest.mark.parametrize("prefix,ranges,n,ok", top.test_check_coverage.pytestmark[0].args[1])

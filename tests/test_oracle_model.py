@@ -127,6 +127,28 @@ def test_causality_prefix_equals_full_rows():
 
 
 @pytest.mark.parametrize("qk_norm", [False, True])
+def test_chunked_prefill_equals_whole_prefill(qk_norm):
+    """A prefix prefilled chunk by chunk (ragged chunks, starts not
+    multiples of 16 or 32) gives the K/V of one prefill over the whole
+    prefix: each chunk's tokens see the earlier chunks through the cache."""
+    cfg = configs.TINY.replace(qk_norm=qk_norm)
+    glob, layers = gen.model_weights(cfg, seed=4, gain_sigma=0.1)
+    g, ls = oracle_weights(glob, layers)
+    shp = shape_of(cfg)
+    ids = gen.token_ids(100, cfg.vocab, seed=4).tolist()
+    Kf, Vf, _ = om.prefill(ids, g, ls, shp)
+    K = [np.zeros((0,) + k.shape[1:]) for k in Kf]
+    V = [np.zeros((0,) + v.shape[1:]) for v in Vf]
+    for a, b in ((0, 37), (37, 38), (38, 80), (80, 100)):
+        kc, vc = om.prefill_chunk(ids[a:b], a, K, V, g, ls, shp)
+        K = [np.concatenate([K[l], kc[l]]) for l in range(cfg.n_layers)]
+        V = [np.concatenate([V[l], vc[l]]) for l in range(cfg.n_layers)]
+    for l in range(cfg.n_layers):
+        np.testing.assert_allclose(K[l], Kf[l], rtol=1e-9, atol=1e-12)
+        np.testing.assert_allclose(V[l], Vf[l], rtol=1e-9, atol=1e-12)
+
+
+@pytest.mark.parametrize("qk_norm", [False, True])
 def test_decode_equals_last_prefill_row(qk_norm):
     cfg = configs.TINY.replace(qk_norm=qk_norm)
     glob, layers = gen.model_weights(cfg, seed=1, gain_sigma=0.1)

@@ -31,6 +31,9 @@ MUTATIONS = [
      "k = qkv[:, Hq * d:(Hq + Hkv) * d].reshape(T, d, Hkv).transpose(0, 2, 1)"),
     ("decode", "K_cache[l][:n], V_cache[l][:n]", "K_cache[l][:n - 1], V_cache[l][:n - 1]"),
     ("decode", "pos = np.array([n])", "pos = np.array([n - 1])"),
+    ("prefill_chunk", "pos = start + np.arange(len(ids))", "pos = np.arange(len(ids))"),
+    ("prefill_chunk", "kp = K_cache[l][:start] if start > 0 else None",
+     "kp = K_cache[l][:start - 1] if start > 1 else None"),
 ]
 
 
@@ -51,6 +54,7 @@ def pins():
     yield to.test_rope_matches_complex_rotation
     yield to.test_rmsnorm_matches_torch
     yield lambda: tm.test_decode_equals_last_prefill_row(True)
+    yield lambda: tm.test_chunked_prefill_equals_whole_prefill(False)
 
 
 @pytest.mark.parametrize("name,old,new", MUTATIONS, ids=[f"{m[0]}-{i}" for i, m in enumerate(MUTATIONS)])
