@@ -51,21 +51,28 @@ typedef __attribute__((address_space(3))) void lds_void;
 // 4-bank groups.
 __device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 7)); }
 
+// One operand tile's K-step into LDS: kLoads instructions per loader wave;
+// instruction i fills slots [(wave*kLoads+i)*64, +64).  voff[i] is the
+// lane's row offset plus its chunk's column offset, or `limit` for a row
+// past the matrix (the range check then returns zeros).  Without a K tail
+// the step's column offset goes into the scalar offset, so a step costs no
+// vector instructions; with one (K not a multiple of BK) each lane checks
+// its column against K.
+template <bool kTail>
 __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
-                                              const int* row_off_valid, const int* chunk, int k0,
-                                              int K, u32x4* lds_tile, int wave, int lane) {
-  // kLoads instructions per loader wave; instruction i fills slots
-  // [(wave*kLoads+i)*64, +64).
+                                              const uint32_t* voff, const int* kcol, int k0,
+                                              int K, u32x4* lds_tile, int wave) {
 #pragma unroll
   for (int i = 0; i < kLoads; ++i) {
-    const int base = (wave * kLoads + i) * 64;
-    const int k = k0 + chunk[i] * 8;
-    const uint32_t off = (row_off_valid[i] >= 0 && k < K)
-                             ? static_cast<uint32_t>(row_off_valid[i]) + static_cast<uint32_t>(k) * 2u
-                             : limit;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_tile + base), 16, off, 0, 0, 0);
+    lds_void* dst = (lds_void*)(lds_tile + (wave * kLoads + i) * 64);
+    if (kTail) {
+      const uint32_t off = (voff[i] < limit && kcol[i] < K - k0) ? voff[i] + static_cast<uint32_t>(k0) * 2u
+                                                                 : limit;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, off, 0, 0, 0);
+    } else {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[i], k0 * 2, 0, 0);
+    }
   }
-  (void)lane;
 }
 
 template <int EPI>
@@ -80,8 +87,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   const int bid = blockIdx.x;
   const int loc = bid / kXcds;
   if (loc >= p.tiles_per_xcd) return;
-  const int t = (bid % kXcds) * p.tiles_per_xcd + loc;
-  if (t >= p.total_tiles) return;
+  const int u = (bid % kXcds) * p.tiles_per_xcd + loc;   // work unit: (tile, K split)
+  if (u >= p.total_tiles * p.ksplit) return;
+  const int t = u / p.ksplit, ks = u % p.ksplit;
   // Grouped order: runs of group_m M-tiles, M fastest, so the ~32
   // workgroups an XCD runs at once cover about group_m x (32 / group_m)
   // tiles and share both operand panels in its L2.
@@ -93,19 +101,22 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   const int m0 = tm * BM;
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5, l32 = lane & 31;
 
-  // Per-thread load plan: row byte offsets (or -1 when out of range) and
-  // source chunk of the LDS slot each load instruction fills.
-  int a_off[kLoads], b_off[kLoads], chunk[kLoads];
+  // Per-thread load plan: byte offset of the row and column chunk each
+  // load instruction fills (or the range limit for a row past the matrix),
+  // and that chunk's first column.
+  uint32_t a_off[kLoads], b_off[kLoads];
+  int kcol[kLoads];
 #pragma unroll
   for (int i = 0; i < kLoads; ++i) {
     const int s = (wave * kLoads + i) * 64 + lane;
     const int row = s / kChunks;
-    chunk[i] = (s % kChunks) ^ ((row >> 1) & 7);
+    const int chunk = (s % kChunks) ^ ((row >> 1) & 7);
+    kcol[i] = chunk * 8;
     const int gm = m0 + row;
-    a_off[i] = gm < p.M ? gm * p.lda * 2 : -1;
+    a_off[i] = gm < p.M ? static_cast<uint32_t>(gm * p.lda * 2 + chunk * 16) : p.a_bytes;
     int gn;
     bool ok;
     if (EPI == kEpiSwiGLU) {
@@ -117,7 +128,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
       gn = tn * BN + row;
       ok = gn < p.N;
     }
-    b_off[i] = ok ? gn * p.ldb * 2 : -1;
+    b_off[i] = ok ? static_cast<uint32_t>(gn * p.ldb * 2 + chunk * 16) : p.b_bytes;
   }
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)p.A, 0, p.a_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)p.B, 0, p.b_bytes, 0x00020000);
@@ -137,14 +148,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   for (int j = 0; j < 2; ++j)
     brow[j] = (EPI == kEpiSwiGLU ? j * 128 + wn * 32 : wn * 64 + j * 32) + l32;
 
-  const int KT = (p.K + BK - 1) / BK;
+  // K steps [kt0, kt0 + KT) of this unit: the whole K range, or split ks
+  // of ksplit near-equal parts.
+  const int KT_all = (p.K + BK - 1) / BK;
+  const int kt0 = ks * KT_all / p.ksplit;
+  const int KT = (ks + 1) * KT_all / p.ksplit - kt0;
+  const int kb = kt0 * BK;
   // Prologue: steps 0 and 1 in flight; then step 0 resident.
   if (wave < kLoaderWaves) {
-    load_tile_lds(ra, p.a_bytes, a_off, chunk, 0, p.K, lds[0][0], wave, lane);
-    load_tile_lds(rb, p.b_bytes, b_off, chunk, 0, p.K, lds[0][1], wave, lane);
+    load_tile_lds<true>(ra, p.a_bytes, a_off, kcol, kb, p.K, lds[0][0], wave);
+    load_tile_lds<true>(rb, p.b_bytes, b_off, kcol, kb, p.K, lds[0][1], wave);
     if (KT > 1) {
-      load_tile_lds(ra, p.a_bytes, a_off, chunk, BK, p.K, lds[1][0], wave, lane);
-      load_tile_lds(rb, p.b_bytes, b_off, chunk, BK, p.K, lds[1][1], wave, lane);
+      load_tile_lds<true>(ra, p.a_bytes, a_off, kcol, kb + BK, p.K, lds[1][0], wave);
+      load_tile_lds<true>(rb, p.b_bytes, b_off, kcol, kb + BK, p.K, lds[1][1], wave);
     }
   }
   if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads) : "memory");
@@ -197,9 +213,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   // (kRefill) go there at once, between the last substep's MFMAs, which
   // also overlap the reads of step kt+1's first substep.  The steady loop
   // has no branches so the LDS reads interleave with the MFMAs.
-  auto step = [&](int kt, auto refill_tag, auto loader_tag) {
+  auto step = [&](int kt, auto refill_tag, auto loader_tag, auto tail_tag) {
     constexpr bool kRefill = decltype(refill_tag)::value;
     constexpr bool kLoader = decltype(loader_tag)::value;
+    constexpr bool kTail = decltype(tail_tag)::value;
     const int slot = kt & 1;
 #pragma unroll
     for (int kk = 0; kk < KK - 1; ++kk) {
@@ -210,8 +227,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     if (kRefill && kLoader) {
-      load_tile_lds(ra, p.a_bytes, a_off, chunk, (kt + 2) * BK, p.K, lds[slot][0], wave, lane);
-      load_tile_lds(rb, p.b_bytes, b_off, chunk, (kt + 2) * BK, p.K, lds[slot][1], wave, lane);
+      load_tile_lds<kTail>(ra, p.a_bytes, a_off, kcol, kb + (kt + 2) * BK, p.K, lds[slot][0], wave);
+      load_tile_lds<kTail>(rb, p.b_bytes, b_off, kcol, kb + (kt + 2) * BK, p.K, lds[slot][1], wave);
     }
     // Step kt+1 is resident; its slot index is valid even past the end
     // (the fragments are then unused).
@@ -222,17 +239,46 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   };
   // The K-loop is specialised per role so the loader waves' loads sit in
   // the same scheduling region as their MFMAs.
-  auto main_loop = [&](auto loader_tag) {
+  auto main_loop = [&](auto loader_tag, auto tail_tag) {
     int kt = 0;
-    for (; kt + 2 < KT; ++kt) step(kt, std::true_type{}, loader_tag);
-    for (; kt < KT; ++kt) step(kt, std::false_type{}, loader_tag);
+    for (; kt + 2 < KT; ++kt) step(kt, std::true_type{}, loader_tag, tail_tag);
+    for (; kt < KT; ++kt) step(kt, std::false_type{}, loader_tag, tail_tag);
   };
-  if (wave < kLoaderWaves) main_loop(std::true_type{});
-  else main_loop(std::false_type{});
+  // Only the loader waves issue loads, and only a K that is not a multiple
+  // of BK needs the per-lane column check.
+  if (wave >= kLoaderWaves) main_loop(std::false_type{}, std::false_type{});
+  else if (p.K % BK == 0) main_loop(std::true_type{}, std::false_type{});
+  else main_loop(std::true_type{}, std::true_type{});
 
   // Epilogue.  Accumulator register r of block (i, j) holds
   // row wm*128 + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.
-  if (EPI == kEpiAddF32) {
+  if (p.ksplit > 1) {
+    // Split K: the raw float32 sums go to part[ks][row][B row]; the reduce
+    // kernel adds the splits in order and applies the epilogue.
+    float* P = p.part + static_cast<int64_t>(ks) * p.M * p.part_ld;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int rr = brow[j];  // tile B row (output column) of this lane
+      int col;
+      bool ok;
+      if (EPI == kEpiSwiGLU) {
+        const int o = tn * (BN / 2) + (rr & 127);
+        ok = o < p.N;
+        col = (rr < 128) ? o : p.N + o;
+      } else {
+        col = tn * BN + rr;
+        ok = col < p.N;
+      }
+      if (!ok) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          if (row < p.M) P[static_cast<int64_t>(row) * p.part_ld + col] = acc[i][j][r];
+        }
+    }
+  } else if (EPI == kEpiAddF32) {
     // Residual add through buffer accesses on this tile's rows: out-of-range
     // rows and columns get an offset past the range, so loads read 0 and
     // stores are dropped without a branch.  Written as C[i] += acc, a load
@@ -319,10 +365,47 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   }
 }
 
+// Split-K reduction: C = epilogue(sum over ks of part[ks]), the splits
+// added in order (so the result is the same run to run), four columns per
+// thread.
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* __restrict__ part, int S, int M,
+                                                          int N, int ld, void* C, int ldc) {
+  const int nq = N / 4;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= static_cast<int64_t>(M) * nq) return;
+  const int row = static_cast<int>(idx / nq), c = static_cast<int>(idx % nq) * 4;
+  const int64_t split = static_cast<int64_t>(M) * ld;
+  const float* src = part + static_cast<int64_t>(row) * ld + c;
+  f32x4 a = *reinterpret_cast<const f32x4*>(src);
+  f32x4 up = {};
+  if (EPI == kEpiSwiGLU) up = *reinterpret_cast<const f32x4*>(src + N);
+  for (int ks = 1; ks < S; ++ks) {
+    a += *reinterpret_cast<const f32x4*>(src + ks * split);
+    if (EPI == kEpiSwiGLU) up += *reinterpret_cast<const f32x4*>(src + ks * split + N);
+  }
+  if (EPI == kEpiAddF32) {
+    f32x4* dst = reinterpret_cast<f32x4*>(static_cast<float*>(C) + static_cast<int64_t>(row) * ldc + c);
+    *dst = *dst + a;
+  } else if (EPI == kEpiF32) {
+    *reinterpret_cast<f32x4*>(static_cast<float*>(C) + static_cast<int64_t>(row) * ldc + c) = a;
+  } else {
+    if (EPI == kEpiSwiGLU) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a[e] = a[e] / (1.0f + __expf(-a[e])) * up[e];
+    }
+    u32x2 w;
+    w.x = pack_bf2(a[0], a[1]);
+    w.y = pack_bf2(a[2], a[3]);
+    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(C) + static_cast<int64_t>(row) * ldc + c) = w;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
-                       int ldc, int M, int N, int K, hipStream_t s, unsigned long long* clk) {
+                       int ldc, int M, int N, int K, float* part, size_t part_bytes, hipStream_t s,
+                       unsigned long long* clk) {
   const int64_t brows64 = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
   // byte offsets are 32-bit (buffer addressing): both operands below 2 GiB
   if (int64_t(M) * lda * 2 >= (int64_t(1) << 31) || brows64 * ldb * 2 >= (int64_t(1) << 31) ||
@@ -339,9 +422,16 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   p.ldb = ldb;
   p.ldc = ldc;
   p.tiles_m = (M + BM - 1) / BM;
-  p.tiles_n = epi == kEpiSwiGLU ? (N + BN / 2 - 1) / (BN / 2) : (N + BN - 1) / BN;
+  p.tiles_n = gemm_tiles_n(epi, N);
   p.total_tiles = p.tiles_m * p.tiles_n;
-  p.tiles_per_xcd = (p.total_tiles + kXcds - 1) / kXcds;
+  p.ksplit = gemm_ksplit(epi, M, N, K);
+  p.part = part;
+  p.part_ld = epi == kEpiSwiGLU ? 2 * N : N;
+  if (p.ksplit > 1 && (!part || part_bytes < gemm_split_bytes(epi, M, N, K) || ldc % 4 != 0 ||
+                       (reinterpret_cast<uintptr_t>(part) & 15) != 0 ||
+                       (reinterpret_cast<uintptr_t>(C) & 15) != 0))
+    return hipErrorInvalidValue;
+  p.tiles_per_xcd = (p.total_tiles * p.ksplit + kXcds - 1) / kXcds;
   p.group_m = std::min(p.tiles_m, kGroupM);
   p.a_bytes = static_cast<uint32_t>(int64_t(M) * lda * 2);
   const int64_t brows = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
@@ -354,6 +444,17 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
     case kEpiSwiGLU: gemm_bf16_kernel<kEpiSwiGLU><<<grid, kThreads, 0, s>>>(p); break;
     case kEpiF32: gemm_bf16_kernel<kEpiF32><<<grid, kThreads, 0, s>>>(p); break;
     default: return hipErrorInvalidValue;
+  }
+  if (p.ksplit > 1) {
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    const int64_t threads = int64_t(M) * (N / 4);
+    const int rgrid = static_cast<int>((threads + 255) / 256);
+    switch (epi) {
+      case kEpiBf16: gemm_reduce_kernel<kEpiBf16><<<rgrid, 256, 0, s>>>(part, p.ksplit, M, N, p.part_ld, C, ldc); break;
+      case kEpiAddF32: gemm_reduce_kernel<kEpiAddF32><<<rgrid, 256, 0, s>>>(part, p.ksplit, M, N, p.part_ld, C, ldc); break;
+      case kEpiSwiGLU: gemm_reduce_kernel<kEpiSwiGLU><<<rgrid, 256, 0, s>>>(part, p.ksplit, M, N, p.part_ld, C, ldc); break;
+      case kEpiF32: gemm_reduce_kernel<kEpiF32><<<rgrid, 256, 0, s>>>(part, p.ksplit, M, N, p.part_ld, C, ldc); break;
+    }
   }
   return hipGetLastError();
 }

@@ -54,16 +54,46 @@ struct GemmParams {
   int M, N, K;
   int lda, ldb, ldc;
   int tiles_m, tiles_n, total_tiles, tiles_per_xcd, group_m;
+  int ksplit;           // K-range splits per tile (1: none)
+  float* part;          // split partial sums [ksplit][M][part_ld] (ksplit > 1)
+  int part_ld;          // B rows: N, or 2N for the gate|up product
   uint32_t a_bytes, b_bytes;
   // Clock sampling (profiling only, else null): each workgroup adds its
   // shader-clock cycles, wall-clock ticks and 1 to clk[0], clk[1], clk[2].
   unsigned long long* clk;
 };
 
+// Output-column tiles of one 256-row M tile (gate|up: 128 gate + 128 up
+// columns per tile).
+inline int gemm_tiles_n(int epi, int N) { return epi == kEpiSwiGLU ? (N + 127) / 128 : (N + 255) / 256; }
+
+// K-range splits per tile.  Only GEMMs of a single 256-row M tile split
+// (their few tiles would leave most of the 256 CUs idle): each split keeps
+// at least 8 K-steps of 64 and the splits fill about 256 workgroups.  The
+// factor depends on N and K alone within M <= 256, and is 1 above, so a
+// row's arithmetic is the same in prefills of any two lengths on the same
+// side of 256 rows.
+inline int gemm_ksplit(int epi, int M, int N, int K) {
+  if (M > 256 || N % 4 != 0) return 1;
+  const int tiles = gemm_tiles_n(epi, N), steps = (K + 63) / 64;
+  int s = 256 / tiles;
+  if (s > steps / 8) s = steps / 8;
+  if (s > 16) s = 16;
+  return s < 1 ? 1 : s;
+}
+// Bytes of float32 partial sums a split GEMM needs (0 when it does not split).
+inline size_t gemm_split_bytes(int epi, int M, int N, int K) {
+  const int s = gemm_ksplit(epi, M, N, K);
+  return s > 1 ? size_t(s) * M * (epi == kEpiSwiGLU ? 2 * size_t(N) : size_t(N)) * 4 : 0;
+}
+
 // A bf16 [M][lda] (K columns used), B bf16 [rows][ldb]; K a multiple of 8;
-// A and B 16-byte aligned; M*lda*2 and rows*ldb*2 below 4 GiB.
+// A and B 16-byte aligned; M*lda*2 and rows*ldb*2 below 2 GiB.  When the
+// GEMM splits K (gemm_ksplit > 1), `part` (16-byte aligned, at least
+// gemm_split_bytes) receives the partial sums and a second kernel reduces
+// them into C; ldc must then be a multiple of 4.
 hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
-                       int ldc, int M, int N, int K, hipStream_t s,
+                       int ldc, int M, int N, int K, float* part, size_t part_bytes, hipStream_t s,
                        unsigned long long* clk = nullptr);
 
 }  // namespace pallas

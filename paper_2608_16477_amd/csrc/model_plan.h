@@ -1,8 +1,10 @@
 // Model handle and the per-call plan of the prefill and decode sequences.
 #pragma once
 
+#include <algorithm>
 #include <vector>
 
+#include "kernels.h"
 #include "pallas.h"
 
 struct pallas_model {
@@ -20,7 +22,7 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Workspace carve-up for `tokens` rows (prefill: sum of prefix lengths;
 // decode: number of sequences).
 struct Workspace {
-  size_t resid, h, qkv, q, o, act, rope, part, total;
+  size_t resid, h, qkv, q, o, act, rope, part, split, split_bytes, total;
 };
 
 // Decode positions are below this bound; decode attention keeps one partial
@@ -41,6 +43,19 @@ inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens, 
   w.act = take(size_t(tokens) * c.ffn * 2);
   w.rope = take(size_t(tokens) * (c.head_dim / 2) * 8);  // (cos, sin) per row and pair
   w.part = take(size_t(seqs) * c.n_q_heads * kDecodeMaxSplits * (c.head_dim + 2) * 4);
+  // Split-K partial sums of the projections of up to 256 rows.
+  {
+    const int rows = static_cast<int>(tokens < 256 ? tokens : 256);
+    const int H = c.hidden, QD = c.n_q_heads * c.head_dim, KVD = 2 * c.n_kv_heads * c.head_dim;
+    size_t b = gemm_split_bytes(kEpiBf16, rows, static_cast<int>(qkv), H);
+    b = std::max(b, gemm_split_bytes(kEpiBf16, rows, KVD, H));
+    b = std::max(b, gemm_split_bytes(kEpiAddF32, rows, H, QD));
+    b = std::max(b, gemm_split_bytes(kEpiSwiGLU, rows, c.ffn, H));
+    b = std::max(b, gemm_split_bytes(kEpiAddF32, rows, H, c.ffn));
+    b = std::max(b, gemm_split_bytes(kEpiF32, rows, c.vocab, H));
+    w.split_bytes = b;
+    w.split = take(b);
+  }
   w.total = at;
   return w;
 }

@@ -321,9 +321,9 @@ const uint16_t* u16(const void* p) { return static_cast<const uint16_t*>(p); }
 // Projection of `rows` activation rows: the MFMA GEMM, or the skinny kernel
 // for up to 8 rows.
 hipError_t project(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C, int ldc,
-                   int rows, int N, int K, hipStream_t s) {
+                   int rows, int N, int K, float* split, size_t split_bytes, hipStream_t s) {
   if (rows <= 8) return pallas::launch_gemv(epi, A, lda, B, ldb, C, ldc, rows, N, K, s);
-  return pallas::launch_gemm(epi, A, lda, B, ldb, C, ldc, rows, N, K, s);
+  return pallas::launch_gemm(epi, A, lda, B, ldb, C, ldc, rows, N, K, split, split_bytes, s);
 }
 
 int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const int32_t* ids,
@@ -338,6 +338,8 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
   uint16_t* o = reinterpret_cast<uint16_t*>(ws + w.o);
   uint16_t* act = reinterpret_cast<uint16_t*>(ws + w.act);
   float* rope = reinterpret_cast<float*>(ws + w.rope);
+  float* split = reinterpret_cast<float*>(ws + w.split);
+  const size_t sb = w.split_bytes;
   const int H = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int QKV = (Hq + 2 * Hkv) * d, QD = Hq * d, KVD = 2 * Hkv * d;
 
@@ -381,14 +383,14 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
     if (last) {
       // Only K and V of the last layer reach the cache.
       PALLAS_TRY(PALLAS_K_GEMM_QKV, pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv) + int64_t(QD) * H, H, qkv, KVD, M,
-                                     KVD, H, s), "kv gemm");
+                                     KVD, H, split, sb, s), "kv gemm");
       qp.qkv = qkv;
       qp.qkv_ld = KVD;
       qp.kv_only = 1;
       PALLAS_TRY(PALLAS_K_QKV_EPI, pallas::launch_qkv_rope(qp, rm, M, s), "kv epilogue");
       break;
     }
-    PALLAS_TRY(PALLAS_K_GEMM_QKV, pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, M, QKV, H, s,
+    PALLAS_TRY(PALLAS_K_GEMM_QKV, pallas::launch_gemm(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, M, QKV, H, split, sb, s,
                                                       pallas::profile_clock_slot(PALLAS_K_GEMM_QKV)), "qkv gemm");
     qp.qkv = qkv;
     qp.qkv_ld = QKV;
@@ -397,13 +399,13 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
     PALLAS_TRY(PALLAS_K_ATTN, pallas::launch_attention_prefill(ap, rm, s), "attention");
-    PALLAS_TRY(PALLAS_K_GEMM_O, pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, s,
+    PALLAS_TRY(PALLAS_K_GEMM_O, pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, split, sb, s,
                                                      pallas::profile_clock_slot(PALLAS_K_GEMM_O)), "o gemm");
     PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, M, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(PALLAS_K_GEMM_GATE_UP, pallas::launch_gemm(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, M, F, H, s,
+    PALLAS_TRY(PALLAS_K_GEMM_GATE_UP, pallas::launch_gemm(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, M, F, H, split, sb, s,
                                                          pallas::profile_clock_slot(PALLAS_K_GEMM_GATE_UP)),
                "gate_up gemm");
-    PALLAS_TRY(PALLAS_K_GEMM_DOWN, pallas::launch_gemm(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, M, H, F, s,
+    PALLAS_TRY(PALLAS_K_GEMM_DOWN, pallas::launch_gemm(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, M, H, F, split, sb, s,
                                                         pallas::profile_clock_slot(PALLAS_K_GEMM_DOWN)), "down gemm");
   }
   return PALLAS_OK;
@@ -423,6 +425,8 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
   uint16_t* o = reinterpret_cast<uint16_t*>(ws + w.o);
   uint16_t* act = reinterpret_cast<uint16_t*>(ws + w.act);
   float* rope = reinterpret_cast<float*>(ws + w.rope);
+  float* split = reinterpret_cast<float*>(ws + w.split);
+  const size_t sb = w.split_bytes;
   const int H = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int QKV = (Hq + 2 * Hkv) * d, QD = Hq * d;
 
@@ -460,7 +464,7 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
     const pallas_layer_weights& L = m->layers[l];
     const Planes pl = layer_planes(pool, l);
     if (l > 0) PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.attn_norm), h, B, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, B, QKV, H, s), "qkv proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, B, QKV, H, split, sb, s), "qkv proj");
     qp.q_gain = u16(L.q_norm);
     qp.k_gain = u16(L.k_norm);
     qp.k_plane = pl.k;
@@ -469,13 +473,13 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
     PALLAS_TRY(PALLAS_K_DECODE_ATTN, pallas::launch_attention_decode(ap, rm, part, pallas::kDecodeMaxSplits, s), "decode attention");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, s), "o proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, split, sb, s), "o proj");
     PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, B, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, s), "gate_up proj");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, B, H, F, s), "down proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, split, sb, s), "gate_up proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, B, H, F, split, sb, s), "down proj");
   }
   PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(m->final_norm), h, B, H, c.rms_eps, s), "final norm");
-  PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiF32, h, H, u16(m->lm_head), H, logits, c.vocab, B, c.vocab, H, s), "lm_head");
+  PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiF32, h, H, u16(m->lm_head), H, logits, c.vocab, B, c.vocab, H, split, sb, s), "lm_head");
   return PALLAS_OK;
 }
 
