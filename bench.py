@@ -315,6 +315,15 @@ def chunked_prefill(st, chunk=256, residents=(0, 1, 2, 3), reps=3, resident_ctx=
         else:
             row["resident_decode_step_ms"] = float(np.median(itl))
         out["rows"].append(row)
+    # one more pass without residents, with events around every launch
+    P.pallas_profile_reset()
+    P.pallas_profile_enable(P.KERNEL_CLASSES)
+    run(0)
+    torch.cuda.synchronize()
+    prof = P.pallas_profile_read()
+    P.pallas_profile_enable([])
+    P.pallas_profile_reset()
+    out["kernels_ms"] = {k: v[0] for k, v in prof.items() if v[1]}
     torch.cuda.synchronize()
     assert int(err.item()) == 0, "device-side error flag raised in the chunked prefill"
     return out

@@ -35,6 +35,7 @@ constexpr float kLazyLog2 = 8.f;  // lazy-rescale headroom, log2 units
 
 struct AttnSched {
   int32_t total;
+  int32_t split_tiles;           // key tiles per split (split launches)
   int32_t prefix[kMaxSeqs + 1];  // query blocks before sequence s
 };
 
@@ -49,8 +50,14 @@ __device__ __forceinline__ float xhalf_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int G>
-__global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowMap rm, AttnSched sch) {
+// kSplit: the key tiles of a query block are divided over gridDim.z
+// workgroups of at most sch.split_tiles tiles each; a workgroup writes its
+// unnormalised output, running max and sum to `part`, and
+// attn_prefill_combine_kernel merges them.  Used when a call has too few
+// query blocks to fill the chip (a 256-token chunk over a long prefix).
+template <int D, int G, bool kSplit>
+__global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowMap rm, AttnSched sch,
+                                                              float* __restrict__ part) {
   constexpr int CH = D / 8;                   // 16-byte chunks per K/V row
   constexpr int ITEMS = (KB / 2) * CH;        // (key pair, chunk) staging items per tile
   constexpr int VROW = KB + VPAD;
@@ -96,11 +103,29 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
   }
 
   const int kend = min(q0 + QB, base + len);
-  const int ntiles = (kend + KB - 1) / KB;
+  const int ntiles_all = (kend + KB - 1) / KB;
+  // This workgroup's key tiles [t0, t0 + ntiles).
+  const int t0 = kSplit ? static_cast<int>(blockIdx.z) * sch.split_tiles : 0;
+  const int ntiles = kSplit ? min(sch.split_tiles, ntiles_all - t0) : ntiles_all;
+  // Split record of (row, head, split): D unnormalised outputs, then the
+  // log2-domain max and the sum of this split's probabilities (D + 4
+  // floats, so records stay 16-byte aligned).
+  float* rec = nullptr;
+  if (kSplit)
+    rec = part + ((static_cast<int64_t>(row0 + (qvalid ? qpos : base)) * p.Hq + h) * gridDim.z + blockIdx.z) * (D + 4);
+  if (kSplit && ntiles <= 0) {
+    // Nothing of this block's keys falls in this split.
+    if (qvalid && g == 0) {
+      rec[D] = -INFINITY;
+      rec[D + 1] = 0.f;
+    }
+    return;
+  }
+  const int kt0 = t0 * KB;
   {
-    // This sequence's block-table entries for keys [0, kend), read once.
-    const int npages = (kend + kPage - 1) / kPage;
-    for (int i = threadIdx.x; i < npages; i += nthreads) bts[i] = bt[i];
+    // This workgroup's block-table entries (keys [kt0, kend)), read once.
+    const int pend = min((kt0 + ntiles * KB + kPage - 1) / kPage, (kend + kPage - 1) / kPage);
+    for (int i = kt0 / kPage + static_cast<int>(threadIdx.x); i < pend; i += nthreads) bts[i] = bt[i];
     __syncthreads();
   }
 
@@ -247,16 +272,16 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
 
   // Pipeline: while tile j's softmax runs, tile j+1's scores are computed
   // from its K tile (already in LDS); K is staged two tiles ahead, V one.
-  gload(skr, kbase, 0);
-  gload(svr, vbase, 0);
+  gload(skr, kbase, kt0);
+  gload(svr, vbase, kt0);
   swriteK(0);
   swriteV(0);
   if (ntiles > 1) {
-    gload(skr, kbase, KB);
+    gload(skr, kbase, kt0 + KB);
     swriteK(1);
-    gload(svr, vbase, KB);
+    gload(svr, vbase, kt0 + KB);
   }
-  if (ntiles > 2) gload(skr, kbase, 2 * KB);
+  if (ntiles > 2) gload(skr, kbase, kt0 + 2 * KB);
   barrier();
   // One pipeline step: scores of tile j+1 into `nxt` while tile j (scores in
   // `cur`, wholly below the diagonal) goes through softmax and PV.
@@ -268,8 +293,8 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
     pv(j & 1, cur);
     if (j + 2 < ntiles) swriteK(j & 1);
     swriteV((j + 1) & 1);
-    if (j + 3 < ntiles) gload(skr, kbase, (j + 3) * KB);
-    if (j + 2 < ntiles) gload(svr, vbase, (j + 2) * KB);
+    if (j + 3 < ntiles) gload(skr, kbase, kt0 + (j + 3) * KB);
+    if (j + 2 < ntiles) gload(svr, vbase, kt0 + (j + 2) * KB);
   };
   f32x16 sa[2], sb[2];
   scores(0, sa);
@@ -285,8 +310,9 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
   }
   f32x16 (&st)[2] = sa;
   {
-    // Last tile: it holds the diagonal and the sequence end.
-    const int k0 = (ntiles - 1) * KB;
+    // Last tile: it holds the diagonal and the sequence end (the mask is
+    // empty for the last tile of a split before them).
+    const int k0 = kt0 + (ntiles - 1) * KB;
     barrier();
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -302,6 +328,21 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
 
   const float l_tot = xhalf_sum(l_run);
   if (!qvalid) return;
+  if (kSplit) {
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int dv = dt * 32 + rg * 8 + g * 4;
+        *reinterpret_cast<f32x4*>(rec + dv) =
+            f32x4{oacc[dt][rg * 4 + 0], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2], oacc[dt][rg * 4 + 3]};
+      }
+    if (g == 0) {
+      rec[D] = m_ref == -INFINITY ? -INFINITY : m_ref * c;
+      rec[D + 1] = l_tot;
+    }
+    return;
+  }
   const float inv_l = l_tot > 0.f ? 1.f / l_tot : 0.f;
   uint16_t* orow = p.o + (static_cast<int64_t>(row0 + qpos) * p.Hq + h) * D;
 #pragma unroll
@@ -314,6 +355,36 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
       w.y = pack_bf2(oacc[dt][rg * 4 + 2] * inv_l, oacc[dt][rg * 4 + 3] * inv_l);
       *reinterpret_cast<u32x2*>(orow + dv) = w;
     }
+}
+
+// Merge of the split records of prefill attention: for (row, head), with
+// M the largest split max, o = sum_j 2^(m_j - M) o_j / sum_j 2^(m_j - M) l_j.
+// 32 threads per (row, head), four output dimensions each (D = 128; two
+// threads' worth idle at D = 64).
+template <int D>
+__global__ __launch_bounds__(256) void attn_prefill_combine_kernel(const float* __restrict__ part, int rows,
+                                                                   int Hq, int S, uint16_t* __restrict__ o) {
+  const int pair = blockIdx.x * 8 + (threadIdx.x >> 5);
+  const int t = threadIdx.x & 31;
+  if (pair >= rows * Hq) return;
+  const float* rec = part + static_cast<int64_t>(pair) * S * (D + 4);
+  float M = -INFINITY;
+  for (int j = 0; j < S; ++j) M = fmaxf(M, rec[j * (D + 4) + D]);
+  f32x4 acc = {};
+  float L = 0.f;
+  for (int j = 0; j < S; ++j) {
+    const float l = rec[j * (D + 4) + D + 1];
+    if (!(l > 0.f)) continue;
+    const float w = __builtin_amdgcn_exp2f(rec[j * (D + 4) + D] - M);
+    L = fmaf(w, l, L);
+    if (t * 4 < D) acc += w * *reinterpret_cast<const f32x4*>(rec + j * (D + 4) + t * 4);
+  }
+  if (t * 4 >= D) return;
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  u32x2 w;
+  w.x = pack_bf2(acc[0] * inv, acc[1] * inv);
+  w.y = pack_bf2(acc[2] * inv, acc[3] * inv);
+  *reinterpret_cast<u32x2*>(o + static_cast<int64_t>(pair) * D + t * 4) = w;
 }
 
 constexpr int kDecThreads = 256;
@@ -519,7 +590,8 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnParams p, Ro
 
 }  // namespace
 
-hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipStream_t s) {
+hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, float* part, size_t part_bytes,
+                                   hipStream_t s) {
   AttnSched sch;
   sch.prefix[0] = 0;
   int maxlen = 0;
@@ -533,11 +605,22 @@ hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipSt
   if (sch.total == 0) return hipSuccess;
   const int G = p.Hq / p.Hkv;
   if (maxlen > kMaxPrefillLen || p.page != kPage) return hipErrorInvalidValue;
-  dim3 grid(sch.total, p.Hkv);
-#define PALLAS_ATTN_CASE(DD, GG)                                                        \
-  if (p.d == DD && G == GG) {                                                           \
-    attn_prefill_kernel<DD, GG><<<grid, GG * 64, 0, s>>>(p, rm, sch);                   \
-    return hipGetLastError();                                                           \
+  const int rows = rm.cu[rm.n_seqs];
+  const int S = attn_prefill_splits(rows, sch.total * p.Hkv, (maxlen + KB - 1) / KB);
+  sch.split_tiles = (((maxlen + KB - 1) / KB) + S - 1) / S;
+  if (S > 1 && (!part || part_bytes < attn_prefill_split_bytes(rows, p.Hq, p.d)))
+    return hipErrorInvalidValue;
+  dim3 grid(sch.total, p.Hkv, S);
+#define PALLAS_ATTN_CASE(DD, GG)                                                                 \
+  if (p.d == DD && G == GG) {                                                                    \
+    if (S == 1) {                                                                                \
+      attn_prefill_kernel<DD, GG, false><<<grid, GG * 64, 0, s>>>(p, rm, sch, nullptr);          \
+      return hipGetLastError();                                                                  \
+    }                                                                                            \
+    attn_prefill_kernel<DD, GG, true><<<grid, GG * 64, 0, s>>>(p, rm, sch, part);                \
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;                             \
+    attn_prefill_combine_kernel<DD><<<(rows * p.Hq + 7) / 8, 256, 0, s>>>(part, rows, p.Hq, S, p.o); \
+    return hipGetLastError();                                                                    \
   }
   PALLAS_ATTN_CASE(128, 1) PALLAS_ATTN_CASE(128, 2) PALLAS_ATTN_CASE(128, 4) PALLAS_ATTN_CASE(128, 8)
   PALLAS_ATTN_CASE(64, 1) PALLAS_ATTN_CASE(64, 2) PALLAS_ATTN_CASE(64, 4) PALLAS_ATTN_CASE(64, 8)

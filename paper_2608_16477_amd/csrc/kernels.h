@@ -163,9 +163,30 @@ struct AttnParams {
   int Hq, Hkv, d;
   float scale_log2;        // log2(e) / sqrt(d)
 };
-// Causal prefill attention: every row attends to keys of its own sequence at
-// positions <= its own (positions start at base_pos = 0).
-hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, hipStream_t s);
+// Key-range splits of prefill attention.  Only calls of at most 256 rows
+// split (as the GEMMs, so longer prefills keep identical bytes per row),
+// and only when their (query block, KV head) workgroups are too few to fill
+// the chip: up to 8 splits of at least 2 key tiles of 64.
+inline int attn_prefill_splits(int rows, int workgroups, int max_tiles) {
+  if (rows > 256 || workgroups >= 256) return 1;
+  int s = (512 + workgroups - 1) / workgroups;
+  if (s > 8) s = 8;
+  if (s > max_tiles / 2) s = max_tiles / 2;
+  if (s < 1) return 1;
+  const int per = (max_tiles + s - 1) / s;
+  return (max_tiles + per - 1) / per;
+}
+// Bytes of split records the workspace holds for up to `rows` rows:
+// [rows][Hq][8][d + 4] floats.
+inline size_t attn_prefill_split_bytes(int rows, int Hq, int d) {
+  return size_t(rows < 256 ? rows : 256) * Hq * 8 * (d + 4) * 4;
+}
+// Causal prefill attention: row t of sequence s is position base_pos[s] +
+// (t - cu[s]) and attends to keys of its own table at positions <= its
+// own, [0, base_pos[s]) written by earlier calls.  `part` (split records,
+// attn_prefill_split_bytes) is used when the call splits its key ranges.
+hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, float* part, size_t part_bytes,
+                                    hipStream_t s);
 // Decode attention: one row per sequence at position base_pos[s], keys
 // [0, base_pos[s]] through the table, split in runs of 64 keys.  `partial`
 // holds [n_seqs][Hq][max_splits][d + 2] floats; needs

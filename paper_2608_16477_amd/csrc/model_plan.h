@@ -22,7 +22,7 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Workspace carve-up for `tokens` rows (prefill: sum of prefix lengths;
 // decode: number of sequences).
 struct Workspace {
-  size_t resid, h, qkv, q, o, act, rope, part, split, split_bytes, total;
+  size_t resid, h, qkv, q, o, act, rope, part, split, split_bytes, attn_split, attn_split_bytes, total;
 };
 
 // Decode positions are below this bound; decode attention keeps one partial
@@ -56,6 +56,10 @@ inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens, 
     w.split_bytes = b;
     w.split = take(b);
   }
+  // Split records of prefill attention over up to 256 rows.
+  w.attn_split_bytes = attn_prefill_split_bytes(static_cast<int>(tokens < 256 ? tokens : 256),
+                                                c.n_q_heads, c.head_dim);
+  w.attn_split = take(w.attn_split_bytes);
   w.total = at;
   return w;
 }

@@ -398,7 +398,8 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
     PALLAS_TRY(PALLAS_K_QKV_EPI, pallas::launch_qkv_rope(qp, rm, M, s), "qkv epilogue");
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
-    PALLAS_TRY(PALLAS_K_ATTN, pallas::launch_attention_prefill(ap, rm, s), "attention");
+    PALLAS_TRY(PALLAS_K_ATTN, pallas::launch_attention_prefill(ap, rm, reinterpret_cast<float*>(ws + w.attn_split),
+                                                               w.attn_split_bytes, s), "attention");
     PALLAS_TRY(PALLAS_K_GEMM_O, pallas::launch_gemm(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, M, H, QD, split, sb, s,
                                                      pallas::profile_clock_slot(PALLAS_K_GEMM_O)), "o gemm");
     PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, M, H, c.rms_eps, s), "rmsnorm");

@@ -16,6 +16,7 @@ import torch
 from helpers import (TOL, empty_pool, ensure_lib, gpu_model, kv_logical, oracle_weights,
                      rel_err, shape_of)
 from oracle import model as om
+from oracle import numerics as on
 from workloads import configs, gen
 
 pytestmark = pytest.mark.gpu
@@ -36,15 +37,31 @@ def chunked(model, cfg, ids, bounds, bt, pool, err):
                             d_bt, pool, ws, err)
 
 
-def check(cfg, glob, layers, ids, pool, bt, n_layers=None):
+def check(cfg, glob, layers, ids, pool, bt, n_layers=None, drift_bound=False):
+    """Oracle parity per (layer, K|V).  With drift_bound the bound of a
+    layer is max(1e-2, 2 x the running maximum of the drift of the oracle's
+    own float32 evaluation from its float64 one) -- the depth reading of
+    the tolerance, for prefixes where bf16 rounding decisions taken from
+    float32 and float64 values already differ at layer 1."""
     g, ls = oracle_weights(glob, layers)
     L = cfg.n_layers if n_layers is None else n_layers
-    K, V, _ = om.prefill(list(ids), g, ls, shape_of(cfg), n_layers=L)
+    shp = shape_of(cfg)
+    K, V, _ = om.prefill(list(ids), g, ls, shp, n_layers=L)
+    bound = [TOL] * L
+    if drift_bound:
+        with om.precision(np.float32):
+            g32 = {k: v.astype(np.float32) for k, v in g.items()}
+            ls32 = [{k: v.astype(np.float32) for k, v in w.items()} for w in ls]
+            K32, V32, _ = om.prefill(list(ids), g32, ls32, shp, rnd=on.bf16_round_as, n_layers=L)
+        worst = 0.0
+        for l in range(L):
+            worst = max(worst, rel_err(K32[l], K[l]), rel_err(V32[l], V[l]))
+            bound[l] = max(TOL, 2.0 * worst)
     lv = kv_logical(pool, bt, len(ids))
     for l in range(L):
         for kv, ref in ((0, K[l]), (1, V[l])):
             e = rel_err(lv[l, kv], ref)
-            assert e <= TOL, f"layer {l} {'KV'[kv]}: rel err {e:.3g}"
+            assert e <= bound[l], f"layer {l} {'KV'[kv]}: rel err {e:.3g} (bound {bound[l]:.3g})"
 
 
 @pytest.mark.parametrize("qk_norm", [False, True])
@@ -78,6 +95,34 @@ def test_mid_layer_shape_256_token_chunks(P):
     torch.cuda.synchronize()
     assert int(err.item()) == 0
     check(cfg, glob, layers, ids, pool, bt)
+
+
+def test_short_chunks_over_long_prefix(P):
+    """Chunks of at most 256 rows after a long first chunk: their query
+    blocks are too few to fill the chip, so attention splits each block's
+    keys over several workgroups (blocks with fewer key tiles than the
+    longest leave their last splits empty) and merges the splits."""
+    cfg = configs.MID.replace(n_layers=2, vocab=4096, name="mid-L2")
+    glob, layers = gen.model_weights(cfg, seed=9, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    n = 900
+    ids = gen.token_ids(n, cfg.vocab, seed=9).numpy()
+    bt = gen.block_table(57, 64, 57, 9, 2)
+    pool = empty_pool(cfg, 64, fill_bits=0x7FA5)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    chunked(model, cfg, ids, [(0, 640), (640, 840), (840, 841), (841, 900)], bt, pool, err)
+    whole = empty_pool(cfg, 64, fill_bits=0x7FA5)
+    chunked(model, cfg, ids, [(0, n)], bt, whole, err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    # At 900 tokens the whole-prefix prefill itself sits at 1.1e-2 on layer
+    # 1's K (position 193, in the first chunk): the depth reading applies.
+    check(cfg, glob, layers, ids, pool, bt, drift_bound=True)
+    # The split rows against the same rows of one undivided prefill.
+    a, b = kv_logical(pool, bt, n)[:, :, 640:], kv_logical(whole, bt, n)[:, :, 640:]
+    for l in range(cfg.n_layers):
+        for kv in (0, 1):
+            assert rel_err(a[l, kv], b[l, kv]) <= TOL
 
 
 def test_several_sequences_at_different_starts(P):
