@@ -77,6 +77,8 @@ def parse():
     ap.add_argument("--no-chunked", action="store_true",
                     help="skip the chunked-prefill measurements (256-token chunks, with 0-3 "
                          "resident decode sessions interleaved)")
+    ap.add_argument("--no-staging", action="store_true",
+                    help="skip the pinned-host staging legs and the two-stream overlap measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device-to-device copy and exit (the reference "
                          "point for scaling FETCH_SIZE / WRITE_SIZE counter readings)")
@@ -329,6 +331,113 @@ def chunked_prefill(st, chunk=256, residents=(0, 1, 2, 3), reps=3, resident_ctx=
     return out
 
 
+def wire_staging(st, reps=10):
+    """The transfer boundary through host memory: the suffix packed on the
+    source side, copied to pinned host memory, copied back to a target-side
+    device arena and assembled -- once as one chunk holding the whole suffix
+    and once for a single 32-token chunk.  Per leg: median time of `reps`
+    runs (HIP events on the current stream) and its rate over the chunk's
+    payload bytes (each leg moves the payload once); the PCIe-inclusive rate
+    is the payload over the sum of the legs."""
+    import numpy as np
+    import torch
+
+    P, cfg = st.P, st.cfg
+    stream = torch.cuda.current_stream()
+    n, p = st.ns[0], st.ps[0]
+    out = {}
+    for name, count in (("suffix", n - p), ("chunk32", 32)):
+        nbytes = count * st.row_bytes
+        src_arena = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        dst_arena = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        desc = [P.ChunkDesc(p, count, 0)]
+        hdr = [P.ChunkHeader(1000, 1, p, count, 0, cfg.n_layers, cfg.n_kv_heads, cfg.head_dim, 2)]
+        legs = {"pack": lambda: P.pallas_pack_suffix_blocks(st.src, st.src_tab[0], desc, src_arena, st.err),
+                "d2h": lambda: host.copy_(src_arena, non_blocking=True),
+                "h2d": lambda: dst_arena.copy_(host, non_blocking=True),
+                "assemble": lambda: P.pallas_assemble_kv(st.dst, st.dst_tab[0], hdr, dst_arena, 1000, 1,
+                                                         st.err)}
+        times = {k: [] for k in legs}
+        for it in range(reps + 2):
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(legs) + 1)]
+            evs[0].record(stream)
+            for i, f in enumerate(legs.values()):
+                f()
+                evs[i + 1].record(stream)
+            torch.cuda.synchronize()
+            if it >= 2:
+                for i, k in enumerate(legs):
+                    times[k].append(evs[i].elapsed_time(evs[i + 1]))
+        row = {"tokens": count, "bytes": nbytes}
+        total = 0.0
+        for k, v in times.items():
+            ms = float(np.median(v))
+            total += ms
+            row[f"{k}_us"] = ms * 1e3
+            row[f"{k}_payload_GBps"] = nbytes / ms / 1e6
+        row["pcie_inclusive_GBps"] = nbytes / total / 1e6
+        assert torch.equal(src_arena, dst_arena)
+        out[name] = row
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    return out
+
+
+def overlapped_preparation(st, chunk=32, reps=3):
+    """Prefix prefill on one stream while the suffix is assembled chunk by
+    chunk (one launch per `chunk` tokens) on another: the time of each alone
+    and of both together, from events on the two streams (median of
+    `reps`)."""
+    import numpy as np
+    import torch
+
+    P, cfg = st.P, st.cfg
+    n, p = st.ns[0], st.ps[0]
+    hdrs = [P.ChunkHeader(1000, 1, t, min(chunk, n - t), (t - p) * st.row_bytes, cfg.n_layers,
+                          cfg.n_kv_heads, cfg.head_dim, 2) for t in range(p, n, chunk)]
+    P.pallas_pack_suffix_blocks(st.src, st.src_tab[0], [P.ChunkDesc(h.start_pos, h.num_tokens, h.arena_offset)
+                                                        for h in hdrs], st.arena, st.err)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def prefill():
+        st.model.prefill_prefix(st.prefix_ids[:p], [0, p], st.dst_tab[:1], st.dst, st.ws, st.err, stream=sa)
+
+    def assemble():
+        for h in hdrs:
+            P.pallas_assemble_kv(st.dst, st.dst_tab[0], [h], st.arena, 1000, 1, st.err, stream=sb)
+
+    def timed(do_prefill, do_assemble):
+        e = {k: torch.cuda.Event(enable_timing=True) for k in ("a0", "a1", "b0", "b1")}
+        torch.cuda.synchronize()
+        e["a0"].record(sa)
+        e["b0"].record(sb)
+        if do_prefill:
+            prefill()
+        if do_assemble:
+            assemble()
+        e["a1"].record(sa)
+        e["b1"].record(sb)
+        torch.cuda.synchronize()
+        return e["a0"].elapsed_time(e["a1"]), e["b0"].elapsed_time(e["b1"])
+
+    res = {"prefill_alone": [], "assemble_alone": [], "prefill_together": [], "assemble_together": []}
+    timed(True, True)
+    for _ in range(reps):
+        res["prefill_alone"].append(timed(True, False)[0])
+        res["assemble_alone"].append(timed(False, True)[1])
+        a, b = timed(True, True)
+        res["prefill_together"].append(a)
+        res["assemble_together"].append(b)
+    out = {k + "_ms": float(np.median(v)) for k, v in res.items()}
+    out["chunks"] = len(hdrs)
+    out["chunk_tokens"] = chunk
+    out["prefill_slowdown"] = out["prefill_together_ms"] / out["prefill_alone_ms"]
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    return out
+
+
 def cpu_baseline(setup):
     """The oracle's first decoder layer (float64 numpy) over the workload's
     prefix rows, scaled by the layer count; plus the oracle's pack of the
@@ -525,6 +634,10 @@ def main():
         print("[bench] chunked prefill", file=sys.stderr, flush=True)
         out["chunked_prefill"] = chunked_prefill(st)
         out["chunked_prefill"]["whole_prefix_ms"] = phase_ms["prefill"]
+    if not args.no_staging:
+        print("[bench] wire staging and overlapped preparation", file=sys.stderr, flush=True)
+        out["wire_staging"] = wire_staging(st)
+        out["overlapped_preparation"] = overlapped_preparation(st)
     if not args.no_stress:
         print("[bench] stress-layout copies", file=sys.stderr, flush=True)
         out["copies_stress"] = copies_stress(P, args.seed)
