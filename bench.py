@@ -438,6 +438,29 @@ def overlapped_preparation(st, chunk=32, reps=3):
     return out
 
 
+def scheduler_decision(P, cfg, prefix_tokens, prefill_ms, assemble_ms, decode_ms, calls=20000):
+    """The Scheduler Engine fed with this run's measurements: r_p = the
+    measured prefix-prefill rate, r_d = one token per measured decode step,
+    T_0 = the measured assembly plus decode step, s_kv of the model; the
+    goodput is the paper's representative 300 Mbps (context, not measured
+    here), alpha 0.8, T_max 5 s, a 10 ms grid, 5 s predicted to handover.
+    Reports the selected window and the mean time of one decision through
+    the binding (ctypes call included)."""
+    params = dict(r_p=prefix_tokens / (prefill_ms / 1e3), r_d=1e3 / decode_ms, goodput=300e6 / 8,
+                  s_kv=float(cfg.s_kv), t_load=0.0, t_0=(assemble_ms + decode_ms) / 1e3, alpha=0.8,
+                  t_max=5.0, dt=0.01)
+    k_curr, t_remain = float(prefix_tokens), 5.0
+    d = P.pallas_window_select(k_curr, t_remain, **params)
+    t0 = time.perf_counter()
+    for _ in range(calls):
+        P.pallas_window_select(k_curr, t_remain, **params)
+    us = (time.perf_counter() - t0) / calls * 1e6
+    return {"inputs": {**params, "k_curr": k_curr, "t_remain": t_remain},
+            "t_w": d.t_w, "t_sit_s": d.t_sit, "t_early_s": d.t_early, "t_hist_s": d.t_hist,
+            "t_res_s": d.t_res, "trigger": bool(d.trigger), "candidates": d.n_candidates,
+            "decision_us": us}
+
+
 def cpu_baseline(setup):
     """The oracle's first decoder layer (float64 numpy) over the workload's
     prefix rows, scaled by the layer count; plus the oracle's pack of the
@@ -634,6 +657,8 @@ def main():
         print("[bench] chunked prefill", file=sys.stderr, flush=True)
         out["chunked_prefill"] = chunked_prefill(st)
         out["chunked_prefill"]["whole_prefix_ms"] = phase_ms["prefill"]
+    out["scheduler"] = scheduler_decision(P, cfg, st.ps[0] if wl.num_seqs == 1 else prefix_tokens,
+                                          phase_ms["prefill"], phase_ms["assemble"], phase_ms["decode"])
     if not args.no_staging:
         print("[bench] wire staging and overlapped preparation", file=sys.stderr, flush=True)
         out["wire_staging"] = wire_staging(st)

@@ -18,6 +18,8 @@
  *   pallas_assemble_kv         scatter chunks into the target block table
  *   pallas_decode_step         one decode step over an assembled cache
  *   pallas_check_coverage      host-only [0, n) coverage check
+ *   pallas_window_*, pallas_ewma_update, pallas_admit, pallas_waste_bound
+ *                              host-only Scheduler Engine (when to migrate)
  *
  * Conventions shared by every call:
  *   - Device pointers are named d_*, host pointers h_*.  All device memory
@@ -256,6 +258,79 @@ int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_token
  * n_ranges > 0 or negative lengths. */
 int pallas_check_coverage(int32_t prefix_len, const int32_t* h_starts, const int32_t* h_lens,
                           int32_t n_ranges, int32_t n);
+
+/* ------------------------------------------------------------------------
+ * Scheduler Engine (host only, no GPU): when to start preparation.
+ *
+ * The prefetching-window model (Section 4.1, Eqs. 3-8) and its online
+ * selection (Section 4.2, Eq. 9 and Algorithm 1).  For a candidate window
+ * T_w (seconds before the predicted handover at which preparation starts),
+ * with K_curr tokens in the context now and T_remain seconds predicted to
+ * handover:
+ *   L_hist  = K_curr + r_d (T_remain - T_w)          prefix at the trigger (Eq. 9)
+ *   T_hist  = T_load + L_hist / r_p                   prefix reconstruction (Eq. 4)
+ *   S_inc   = r_d T_w s_kv                            suffix bytes in the window (Eq. 3)
+ *   T_res   = max(0, S_inc / B - T_w)                 suffix backlog at handover (Eq. 5)
+ *   T_SIT   = T_0 + max(0, T_hist - T_w, T_res)       service interruption (Eq. 6)
+ *   T_early = max(0, T_w - T_hist)                    early-preparation exposure (Eq. 7)
+ *   J       = alpha T_SIT + (1 - alpha) T_early       objective (Eq. 8)
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  double r_p;     /* prefill throughput available to the migration at the target, tokens/s (> 0) */
+  double r_d;     /* source-side decode throughput of the request, tokens/s (>= 0) */
+  double goodput; /* inter-gNB goodput B available to the migration, bytes/s (> 0) */
+  double s_kv;    /* KV-cache bytes per token, Eq. 1 (>= 0) */
+  double t_load;  /* model load time at the target, s (>= 0; 0 when resident) */
+  double t_0;     /* window-independent activation latency, s (>= 0) */
+  double alpha;   /* objective weight in [0, 1] */
+  double t_max;   /* largest window considered, s (>= 0) */
+  double dt;      /* candidate grid step, s (> 0) */
+} pallas_window_params;
+
+typedef struct {
+  double t_w;     /* the window */
+  double cost;    /* J(t_w) */
+  double t_sit;   /* T_SIT(t_w) */
+  double t_early; /* T_early(t_w) */
+  double t_hist;  /* T_hist(t_w) */
+  double t_res;   /* T_res(t_w) */
+  double l_hist;  /* L_hist(t_w), tokens */
+  int32_t n_candidates; /* windows evaluated (selection only) */
+  int32_t trigger;      /* selection only: 1 when T_remain <= t_w (start now), else 0 (defer) */
+} pallas_window_decision;
+
+/* The model at one window t_w (>= 0).  INVALID_ARG on a null pointer or a
+ * parameter outside its range. */
+int pallas_window_evaluate(const pallas_window_params* p, double k_curr, double t_remain, double t_w,
+                           pallas_window_decision* out);
+
+/* Algorithm 1's window decision: candidates {0, dt, 2 dt, ...} up to
+ * T_limit = min(t_max, max(T_remain, 0)), plus T_limit itself when it is not
+ * on the grid; the smallest J wins, the smallest window among equal J.
+ * trigger = (T_remain <= t_w).  INVALID_ARG as above, or when the grid
+ * would exceed 10^7 candidates. */
+int pallas_window_select(const pallas_window_params* p, double k_curr, double t_remain,
+                         pallas_window_decision* out);
+
+/* Exponentially weighted moving average of a telemetry rate (Section 4.2:
+ * r_p, r_d and B are smoothed): the first sample sets the value, later
+ * ones move it by `weight` (in (0, 1]) towards the sample.  Returns the new
+ * value (NaN and no change on a null pointer or a weight outside (0, 1]). */
+typedef struct {
+  double value;
+  int32_t primed;
+} pallas_ewma;
+double pallas_ewma_update(pallas_ewma* e, double sample, double weight);
+
+/* Admission (Section 4.2): 1 when the target runs a compatible model and
+ * its free VRAM holds the request state expected at handover,
+ * s_kv (K_curr + r_d max(T_remain, 0)) bytes; else 0. */
+int32_t pallas_admit(int32_t model_compatible, double vram_free_bytes, double s_kv, double k_curr,
+                     double r_d, double t_remain);
+
+/* Bound on preparation discarded after wrong target predictions (Section
+ * 4.4, Eq. 10): max(t_max + e_early - t_avail, 0) seconds. */
+double pallas_waste_bound(double t_max, double e_early, double t_avail);
 
 /* Per-kernel timing (tracing).  Kernel classes of the calls above: */
 typedef enum {

@@ -12,8 +12,11 @@ reconstruction computes, written from the paper:
 * ``paged``     -- the paged KV layout, suffix-block extraction, assembly into
                    a new block table, the coverage and epoch checks
                    (Sections 4.3 and 5).
+* ``scheduler`` -- the prefetching-window model and its online selection,
+                   admission, rate smoothing and the stale-preparation bound
+                   (Sections 4.1, 4.2 and 4.4).
 
 It shares no code with the HIP library or its Python binding.  Inputs
 (weights, ids, tables) come from the seeded generators in ``workloads``.
 """
-from . import footprint, numerics, model, paged  # noqa: F401
+from . import footprint, numerics, model, paged, scheduler  # noqa: F401

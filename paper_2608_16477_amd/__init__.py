@@ -13,4 +13,6 @@ from .binding import (  # noqa: F401
     pallas_prefill_prefix, pallas_prefill_chunk, pallas_pack_suffix_blocks, pallas_assemble_kv,
     pallas_decode_step, Model, ChunkDesc, ChunkHeader, EXPORTS, KERNEL_CLASSES,
     pallas_profile_enable, pallas_profile_read, pallas_profile_reset, pallas_profile_clock,
+    pallas_window_select, pallas_window_evaluate, pallas_ewma_update, pallas_admit,
+    pallas_waste_bound, WindowParams, WindowDecision, Ewma,
 )

@@ -69,6 +69,20 @@ class ChunkHeader(C.Structure):
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("elem_bytes", C.c_int32)]
 
 
+class WindowParams(C.Structure):
+    _fields_ = [(n, C.c_double) for n in ("r_p", "r_d", "goodput", "s_kv", "t_load", "t_0", "alpha",
+                                          "t_max", "dt")]
+
+
+class WindowDecision(C.Structure):
+    _fields_ = [(n, C.c_double) for n in ("t_w", "cost", "t_sit", "t_early", "t_hist", "t_res",
+                                          "l_hist")] + [("n_candidates", C.c_int32), ("trigger", C.c_int32)]
+
+
+class Ewma(C.Structure):
+    _fields_ = [("value", C.c_double), ("primed", C.c_int32)]
+
+
 _vp, _i32, _u64, _sz = C.c_void_p, C.c_int32, C.c_uint64, C.c_size_t
 _pi32 = C.POINTER(C.c_int32)
 
@@ -90,6 +104,13 @@ EXPORTS = {
     "pallas_decode_step": (C.c_int, [_vp, _i32, _vp, _pi32, _vp, _i32, C.POINTER(KVPoolC), _vp,
                                      _vp, _sz, _vp, _vp]),
     "pallas_check_coverage": (C.c_int, [_i32, _pi32, _pi32, _i32, _i32]),
+    "pallas_window_evaluate": (C.c_int, [C.POINTER(WindowParams), C.c_double, C.c_double, C.c_double,
+                                         C.POINTER(WindowDecision)]),
+    "pallas_window_select": (C.c_int, [C.POINTER(WindowParams), C.c_double, C.c_double,
+                                       C.POINTER(WindowDecision)]),
+    "pallas_ewma_update": (C.c_double, [C.POINTER(Ewma), C.c_double, C.c_double]),
+    "pallas_admit": (_i32, [_i32, C.c_double, C.c_double, C.c_double, C.c_double, C.c_double]),
+    "pallas_waste_bound": (C.c_double, [C.c_double, C.c_double, C.c_double]),
     "pallas_profile_enable": (None, [C.c_uint32]),
     "pallas_profile_read": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     "pallas_profile_reset": (None, []),
@@ -238,6 +259,41 @@ def pallas_decode_step(h, tokens, positions: Sequence[int], block_tables, pool, 
                                     _ptr(logits), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _ptr(err),
                                     _stream(stream)))
+
+
+def _window_params(r_p, r_d, goodput, s_kv, t_load=0.0, t_0=0.0, alpha=0.8, t_max=5.0, dt=0.01):
+    return WindowParams(r_p, r_d, goodput, s_kv, t_load, t_0, alpha, t_max, dt)
+
+
+def pallas_window_select(k_curr: float, t_remain: float, **params) -> WindowDecision:
+    """Algorithm 1's window decision; ``params`` are the fields of
+    pallas_window_params (r_p, r_d, goodput, s_kv, t_load, t_0, alpha,
+    t_max, dt)."""
+    p = _window_params(**params)
+    d = WindowDecision()
+    _check(lib().pallas_window_select(C.byref(p), k_curr, t_remain, C.byref(d)))
+    return d
+
+
+def pallas_window_evaluate(k_curr: float, t_remain: float, t_w: float, **params) -> WindowDecision:
+    p = _window_params(**params)
+    d = WindowDecision()
+    _check(lib().pallas_window_evaluate(C.byref(p), k_curr, t_remain, t_w, C.byref(d)))
+    return d
+
+
+def pallas_ewma_update(state: Ewma, sample: float, weight: float) -> float:
+    return lib().pallas_ewma_update(C.byref(state), sample, weight)
+
+
+def pallas_admit(model_compatible: bool, vram_free_bytes: float, s_kv: float, k_curr: float,
+                 r_d: float, t_remain: float) -> bool:
+    return bool(lib().pallas_admit(int(bool(model_compatible)), vram_free_bytes, s_kv, k_curr, r_d,
+                                   t_remain))
+
+
+def pallas_waste_bound(t_max: float, e_early: float, t_avail: float) -> float:
+    return lib().pallas_waste_bound(t_max, e_early, t_avail)
 
 
 def pallas_profile_enable(classes=KERNEL_CLASSES):

@@ -1,6 +1,7 @@
 """Build the gfx950 shared library ``libpallas.so`` in-tree.
 
-Every ``csrc/*.hip`` file is compiled with hipcc for gfx950 and linked into
+Every ``csrc/*.hip`` file is compiled with hipcc for gfx950, every
+``csrc/*.cpp`` file (host-only code) as plain C++, and all are linked into
 one shared library next to this file.  Run ``python -m
 paper_2608_16477_amd.build`` (or ``__graft_entry__.build()``).
 """
@@ -29,13 +30,20 @@ CFLAGS = [
 ]
 
 
+# host-only C++ (the Scheduler Engine): no device code, no offload target
+CXXFLAGS = ["-x", "c++", "-O3", "-fPIC", "-std=c++17", "-I", os.path.join(ROOT, "include"),
+            "-I", CSRC]
+
+
 def sources():
-    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp")))
 
 
 def _compile(src: str) -> str:
-    obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    stem, ext = os.path.splitext(os.path.basename(src))
+    obj = os.path.join(BUILD, stem + ".o")
+    flags = CFLAGS if ext == ".hip" else CXXFLAGS
+    cmd = [HIPCC, *flags, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")
