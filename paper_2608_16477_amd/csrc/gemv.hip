@@ -19,7 +19,6 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
-constexpr int kStages = 3;
 constexpr int kKStep = 64;        // k per stage: one 128-byte line per weight row
 constexpr int kBlockSlots = 68;   // 8 rows x 8 slots of 16 B, plus 4 slots of padding
 
@@ -27,6 +26,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 template <int TILES>
 struct GvLayout {
+  static constexpr int kStages = 3;                                   // stages in flight per wave
   static constexpr int kWBlocks = 2 * TILES;                          // 8-row blocks per stage
   static constexpr int kStageSlots = kWBlocks * kBlockSlots + 64;     // + one X block
   static constexpr int kWaveSlots = kStages * kStageSlots;
@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
   u32x4* wbase = lds + wave * L::kWaveSlots;
   auto issue = [&](int s) {
     const int k0 = kb + s * kKStep;
-    u32x4* st = wbase + (s % kStages) * L::kStageSlots;
+    u32x4* st = wbase + (s % L::kStages) * L::kStageSlots;
 #pragma unroll
     for (int blk = 0; blk < L::kWBlocks; ++blk) {
       const int t = blk >> 1;
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
 #pragma unroll
   for (int t = 0; t < TILES; ++t) acc[t] = f32x4{0, 0, 0, 0};
   auto compute = [&](int s) {
-    const u32x4* st = wbase + (s % kStages) * L::kStageSlots;
+    const u32x4* st = wbase + (s % L::kStages) * L::kStageSlots;
 #pragma unroll
     for (int q = 0; q < kKStep / 32; ++q) {
       const int c = 4 * q + kg;
@@ -120,16 +120,21 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
     }
   };
 
-  for (int s = 0; s < kStages - 1 && s < nst; ++s) issue(s);
+  for (int s = 0; s < L::kStages - 1 && s < nst; ++s) issue(s);
   for (int s = 0; s < nst; ++s) {
     asm volatile("" ::: "memory");
-    if (s + kStages - 1 < nst) {
-      issue(s + kStages - 1);
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kStages - 1) * L::kLoads) : "memory");
-    } else if (s + 1 < nst) {
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L::kLoads) : "memory");
+    if (s + L::kStages - 1 < nst) {
+      issue(s + L::kStages - 1);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((L::kStages - 1) * L::kLoads) : "memory");
     } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // Tail: stages s+1 .. nst-1 may stay in flight.
+      switch (nst - 1 - s) {
+        case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L::kLoads) : "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * L::kLoads) : "memory"); break;
+        case 3: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * L::kLoads) : "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * L::kLoads) : "memory"); break;
+      }
     }
     compute(s);
   }

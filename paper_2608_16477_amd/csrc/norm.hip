@@ -2,7 +2,8 @@
 //
 // RMSNorm: h = bf16(x * (mean(x^2) + eps)^(-1/2) * g) with x the float32
 // residual row; one workgroup per row, float4 loads, a wave64 butterfly sum
-// and a cross-wave sum through LDS.
+// and a cross-wave sum through LDS.  Rows up to 8192 wide are held in
+// registers between the two passes.
 #include "common.h"
 #include "kernels.h"
 
@@ -60,6 +61,35 @@ __global__ __launch_bounds__(kThreads) void embed_rmsnorm_kernel(
   }
 }
 
+// Rows of up to kRegVecs * kThreads * 4 elements stay in registers between
+// the sum of squares and the scaling, so a row is read from memory once.
+constexpr int kRegVecs = 8;
+
+__global__ __launch_bounds__(kThreads) void rmsnorm_reg_kernel(const float* __restrict__ r,
+                                                               const uint16_t* __restrict__ g,
+                                                               uint16_t* __restrict__ h, int H,
+                                                               float eps) {
+  __shared__ float sh[kThreads / 64];
+  const int t = blockIdx.x;
+  const float* rr = r + static_cast<int64_t>(t) * H;
+  f32x4 x[kRegVecs];
+  float ss = 0.f;
+#pragma unroll
+  for (int v = 0; v < kRegVecs; ++v) {
+    const int i = (v * kThreads + threadIdx.x) * 4;
+    x[v] = i < H ? *reinterpret_cast<const f32x4*>(rr + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int v = 0; v < kRegVecs; ++v) ss += x[v].x * x[v].x + x[v].y * x[v].y + x[v].z * x[v].z + x[v].w * x[v].w;
+  const float inv = rsqrtf(block_sum(ss, sh) / H + eps);
+  uint16_t* hh = h + static_cast<int64_t>(t) * H;
+#pragma unroll
+  for (int v = 0; v < kRegVecs; ++v) {
+    const int i = (v * kThreads + threadIdx.x) * 4;
+    if (i < H) store_norm4(hh, g, i, x[v], inv);
+  }
+}
+
 __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const float* __restrict__ r,
                                                            const uint16_t* __restrict__ g,
                                                            uint16_t* __restrict__ h, int H,
@@ -106,7 +136,10 @@ hipError_t launch_embed_rmsnorm(const int32_t* ids, const uint16_t* embed, const
 hipError_t launch_rmsnorm(const float* r, const uint16_t* gain, uint16_t* h, int rows, int H,
                           float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  rmsnorm_kernel<<<rows, kThreads, 0, s>>>(r, gain, h, H, eps);
+  if (H <= kRegVecs * kThreads * 4)
+    rmsnorm_reg_kernel<<<rows, kThreads, 0, s>>>(r, gain, h, H, eps);
+  else
+    rmsnorm_kernel<<<rows, kThreads, 0, s>>>(r, gain, h, H, eps);
   return hipGetLastError();
 }
 

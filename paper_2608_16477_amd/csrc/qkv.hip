@@ -14,6 +14,7 @@ namespace pallas {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kGroup = 5;   // passes whose loads are in flight together
 
 // One workgroup per row.  A lane owns 4 rotary pairs: elements [4j, 4j+4)
 // of the head's first half and their partners [4j+d/2, 4j+d/2+4), loaded as
@@ -39,18 +40,30 @@ __global__ __launch_bounds__(kThreads) void qkv_rope_kernel(QkvParams p, RowMap 
   const uint16_t* src_row = p.qkv + static_cast<int64_t>(row) * p.qkv_ld;
   bool flagged = false;
 
-  for (int h0 = 0; h0 < heads; h0 += HPB) {
-    const int hl = h0 + hsub;                   // local head index
+  // The loads of kGroup passes are issued before any of their stores (the
+  // stores may not alias them, but the compiler cannot know): one memory
+  // round trip per group of passes instead of one per pass.
+  for (int g0 = 0; g0 < heads; g0 += kGroup * HPB) {
+  u32x2 lov[kGroup], hiv[kGroup];
+#pragma unroll
+  for (int ps = 0; ps < kGroup; ++ps) {
+    const int hl = g0 + ps * HPB + hsub;
+    lov[ps] = hiv[ps] = u32x2{0, 0};
+    if (hl < heads) {
+      const uint16_t* src = src_row + static_cast<int64_t>(hl) * D;
+      lov[ps] = *reinterpret_cast<const u32x2*>(src + 4 * j);
+      hiv[ps] = *reinterpret_cast<const u32x2*>(src + HALF + 4 * j);
+    }
+  }
+
+#pragma unroll
+  for (int ps = 0; ps < kGroup; ++ps) {
+    const int hl = g0 + ps * HPB + hsub;        // local head index
     const bool active = hl < heads;
     const int hh = hl + (p.kv_only ? p.Hq : 0); // head in [0, Hq + 2 Hkv)
     const bool is_q = hh < p.Hq;
     const bool is_k = !is_q && hh < p.Hq + p.Hkv;
-    u32x2 lo = {0, 0}, hi = {0, 0};
-    if (active) {
-      const uint16_t* src = src_row + static_cast<int64_t>(hl) * D;
-      lo = *reinterpret_cast<const u32x2*>(src + 4 * j);
-      hi = *reinterpret_cast<const u32x2*>(src + HALF + 4 * j);
-    }
+    const u32x2 lo = lov[ps], hi = hiv[ps];
     float x0[4] = {bflo(lo.x), bfhi(lo.x), bflo(lo.y), bfhi(lo.y)};
     float x1[4] = {bflo(hi.x), bfhi(hi.x), bflo(hi.y), bfhi(hi.y)};
     u32x2 olo = lo, ohi = hi;
@@ -96,6 +109,7 @@ __global__ __launch_bounds__(kThreads) void qkv_rope_kernel(QkvParams p, RowMap 
     }
     *reinterpret_cast<u32x2*>(dst + 4 * j) = olo;
     *reinterpret_cast<u32x2*>(dst + HALF + 4 * j) = ohi;
+  }
   }
   if (flagged && j == 0 && p.err) atomicOr(p.err, static_cast<int32_t>(PALLAS_DEVERR_PAGE));
 }
