@@ -10,6 +10,8 @@
 // operand reads (16 rows at one k) hit 16 distinct bank groups.  The four
 // partial tiles are summed through LDS and the epilogue matches the prefill
 // GEMM's.
+#include <cmath>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -40,27 +42,39 @@ __device__ __forceinline__ int wslot(int rr, int c) {
 // X block slot of (row r in 0..7, chunk c in 0..7).
 __device__ __forceinline__ int xslot(int r, int c) { return r * 8 + (c ^ r); }
 
+// K split over workgroups: workgroup (tile, ks) covers K range ks of S and
+// writes float32 partial sums to part[ks][m][B row]; the last workgroup of
+// a tile to finish (an atomic count in ctr[tile], which it resets to 0)
+// adds the S partials in order and applies the epilogue.
+struct GemvSplit {
+  int S;
+  float* part;   // [S][M][B rows]
+  int* ctr;      // [tiles], zero on entry
+  int nrows;     // B rows: N, or 2N for gate|up
+};
+
 template <int EPI, int TILES>
 __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restrict__ X, int ldx,
                                                         const uint16_t* __restrict__ W, int ldw,
                                                         void* __restrict__ C, int ldc, int M, int N,
-                                                        int K) {
+                                                        int K, GemvSplit sp) {
   using L = GvLayout<TILES>;
   __shared__ __attribute__((aligned(16))) u32x4 lds[kWaves * L::kWaveSlots];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, kg = lane >> 4;
+  const int tile = static_cast<int>(blockIdx.x) / sp.S, ks = static_cast<int>(blockIdx.x) % sp.S;
 
   // Weight tiles: first row and valid row count.
   int trow[TILES], tvalid[TILES];
   if (EPI == kEpiSwiGLU) {
-    const int o0 = blockIdx.x * 16;
+    const int o0 = tile * 16;
     trow[0] = o0;
     trow[TILES - 1] = N + o0;
     tvalid[0] = tvalid[TILES - 1] = min(16, N - o0);
   } else {
 #pragma unroll
     for (int t = 0; t < TILES; ++t) {
-      trow[t] = (blockIdx.x * TILES + t) * 16;
+      trow[t] = (tile * TILES + t) * 16;
       tvalid[t] = max(0, min(16, N - trow[t]));
     }
   }
@@ -73,8 +87,11 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
       __builtin_amdgcn_make_buffer_rsrc((void*)X, 0, static_cast<uint32_t>(M) * ldx * 2u, 0x00020000);
   constexpr uint32_t kOob = 0xFFFFFFF0u;
 
-  const int kslice = ((K + kWaves * kKStep - 1) / (kWaves * kKStep)) * kKStep;
-  const int kb = wave * kslice, ke = min(K, kb + kslice);
+  // This workgroup's K range [kw0, kw1), then a quarter of it per wave.
+  const int kper = ((K + sp.S * kKStep - 1) / (sp.S * kKStep)) * kKStep;
+  const int kw0 = ks * kper, kw1 = min(K, kw0 + kper);
+  const int kslice = ((max(kw1 - kw0, 0) + kWaves * kKStep - 1) / (kWaves * kKStep)) * kKStep;
+  const int kb = kw0 + wave * kslice, ke = min(kw1, kb + kslice);
   const int nst = ke > kb ? (ke - kb + kKStep - 1) / kKStep : 0;
 
   // Per-lane load coordinates (fixed for every stage).
@@ -154,12 +171,49 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
     for (int w = 1; w < kWaves; ++w) sum[t] += red[(w * TILES + t) * 64 + lane];
   }
   // lane holds column li and rows kg*4 + r
+  if (sp.S > 1) {
+    const bool col_ok = (EPI == kEpiSwiGLU ? tile * 16 : trow[0]) + li < N;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = kg * 4 + r;
+      if (m >= M || !col_ok) continue;
+#pragma unroll
+      for (int t = 0; t < TILES; ++t)
+        __hip_atomic_store(sp.part + (static_cast<int64_t>(ks) * M + m) * sp.nrows + trow[t] + li, sum[t][r],
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // The partials are agent-scope stores, which write through the XCD's
+    // L2; once they have completed, the count goes up.  (A device fence
+    // here would write back and invalidate the whole L2 for every
+    // workgroup, which made the kernel four times slower.)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    int prev = 0;
+    if (lane == 0) prev = __hip_atomic_fetch_add(sp.ctr + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    prev = __shfl(prev, 0, kWave);
+    if (prev != sp.S - 1) return;
+    asm volatile("" ::: "memory");
+    // Last of the tile: the others' partials, read past this XCD's L2.
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = kg * 4 + r;
+#pragma unroll
+      for (int t = 0; t < TILES; ++t) {
+        float v = 0.f;
+        if (m < M && col_ok)
+          for (int j = 0; j < sp.S; ++j)
+            v += __hip_atomic_load(sp.part + (static_cast<int64_t>(j) * M + m) * sp.nrows + trow[t] + li,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sum[t][r] = v;
+      }
+    }
+    if (lane == 0) __hip_atomic_store(sp.ctr + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int m = kg * 4 + r;
     if (m >= M) continue;
     if (EPI == kEpiSwiGLU) {
-      const int col = blockIdx.x * 16 + li;
+      const int col = tile * 16 + li;
       if (col < N) {
         const float gt = sum[0][r], up = sum[TILES - 1][r];
         static_cast<uint16_t*>(C)[static_cast<int64_t>(m) * ldc + col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
@@ -179,20 +233,63 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
   }
 }
 
+__global__ void fill_zero_kernel(int* __restrict__ p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
 }  // namespace
 
+int gemv_ksplit(int epi, int N, int K) {
+  // Workgroups per tile, for launches of fewer than two tiles per CU (O and
+  // down at the large shape: 320 tiles): the split whose workgroup count
+  // divides most evenly over the 256 CUs, with at least four 64-wide
+  // K-steps per wave, and only when it beats no split by more than 5%.
+  // Measured at the large shape, M = 1: O 21.6 -> 18.8 us and down 64 ->
+  // 58 us with four splits; Q|K|V (640 tiles) and gate|up (1600) ran 10%
+  // slower split in two, so they do not split.
+  const int tiles = (N + 15) / 16;
+  if (tiles >= 512) return 1;
+  auto eff = [&](int s) {
+    const double per_cu = double(tiles) * s / 256.0;
+    return per_cu / std::ceil(per_cu);
+  };
+  int best = 1;
+  for (int s = 2; s <= kGemvMaxSplit; ++s) {
+    if (K / (s * kWaves * kKStep) < 4) break;
+    if (eff(s) > eff(best) + 0.05) best = s;
+  }
+  return best;
+}
+
+hipError_t launch_zero_counters(int* ctr, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  fill_zero_kernel<<<(n + 255) / 256, 256, 0, s>>>(ctr, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemv(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
-                       int ldc, int M, int N, int K, hipStream_t s) {
+                       int ldc, int M, int N, int K, float* part, size_t part_bytes, int* ctr,
+                       int ctr_count, hipStream_t s) {
   if (M <= 0 || M > 8 || N <= 0 || K <= 0 || (K & 7) || (lda & 7) || (ldb & 7)) return hipErrorInvalidValue;
   // 32-bit buffer offsets: one 16-row weight tile and the X rows
   if (static_cast<int64_t>(16) * ldb * 2 >= (int64_t(1) << 32) || static_cast<int64_t>(8) * lda * 2 >= (int64_t(1) << 32))
     return hipErrorInvalidValue;
   const int tiles = (N + 15) / 16;
+  GemvSplit sp;
+  sp.S = gemv_ksplit(epi, N, K);
+  sp.nrows = epi == kEpiSwiGLU ? 2 * N : N;
+  sp.part = part;
+  sp.ctr = ctr;
+  if (sp.S > 1 && (!part || !ctr || ctr_count < tiles ||
+                   part_bytes < size_t(sp.S) * M * sp.nrows * sizeof(float)))
+    sp.S = 1;   // no room for the split: stream the whole K per tile
+  const int grid = tiles * sp.S;
   switch (epi) {
-    case kEpiBf16: gemv_kernel<kEpiBf16, 1><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
-    case kEpiAddF32: gemv_kernel<kEpiAddF32, 1><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
-    case kEpiF32: gemv_kernel<kEpiF32, 1><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
-    case kEpiSwiGLU: gemv_kernel<kEpiSwiGLU, 2><<<tiles, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K); break;
+    case kEpiBf16: gemv_kernel<kEpiBf16, 1><<<grid, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, sp); break;
+    case kEpiAddF32: gemv_kernel<kEpiAddF32, 1><<<grid, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, sp); break;
+    case kEpiF32: gemv_kernel<kEpiF32, 1><<<grid, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, sp); break;
+    case kEpiSwiGLU: gemv_kernel<kEpiSwiGLU, 2><<<grid, kThreads, 0, s>>>(A, lda, B, ldb, C, ldc, M, N, K, sp); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

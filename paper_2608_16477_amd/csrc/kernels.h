@@ -196,7 +196,16 @@ hipError_t launch_attention_decode(const AttnParams& p, const RowMap& rm, float*
 
 // ------------------------------------------------------------ skinny GEMM
 // C[m][n] (op) A[m] . B[n] for m < M <= 8 rows; epilogues as launch_gemm.
+// With gemv_ksplit(epi, N, K) = S > 1 the K range of each 16-row tile is
+// split over S workgroups: `part` needs S * M * (N, or 2N for gate|up)
+// floats and `ctr` one int per tile, zero on entry and left zero (else, or
+// with too little room, the launch does not split).
+constexpr int kGemvMaxSplit = 8;
+int gemv_ksplit(int epi, int N, int K);
 hipError_t launch_gemv(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
-                       int ldc, int M, int N, int K, hipStream_t s);
+                       int ldc, int M, int N, int K, float* part, size_t part_bytes, int* ctr,
+                       int ctr_count, hipStream_t s);
+// ctr[0..n) = 0 (a kernel, so it can sit in a captured graph).
+hipError_t launch_zero_counters(int* ctr, int n, hipStream_t s);
 
 }  // namespace pallas

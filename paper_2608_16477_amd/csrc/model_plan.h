@@ -22,7 +22,10 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Workspace carve-up for `tokens` rows (prefill: sum of prefix lengths;
 // decode: number of sequences).
 struct Workspace {
-  size_t resid, h, qkv, q, o, act, rope, part, split, split_bytes, attn_split, attn_split_bytes, total;
+  size_t resid, h, qkv, q, o, act, rope, part, split, split_bytes, attn_split, attn_split_bytes;
+  size_t gemv_part, gemv_part_bytes, gemv_ctr;
+  int gemv_ctr_count;
+  size_t total;
 };
 
 // Decode positions are below this bound; decode attention keeps one partial
@@ -60,6 +63,17 @@ inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens, 
   w.attn_split_bytes = attn_prefill_split_bytes(static_cast<int>(tokens < 256 ? tokens : 256),
                                                 c.n_q_heads, c.head_dim);
   w.attn_split = take(w.attn_split_bytes);
+  // Decode projections (at most 8 rows) split over K: partial sums and one
+  // arrival counter per 16-row weight tile.
+  {
+    const int64_t rows = std::max<int64_t>(
+        std::max<int64_t>(qkv, 2 * int64_t(c.ffn)), std::max<int64_t>(c.hidden, c.vocab));
+    const int64_t r8 = std::min<int64_t>(std::min<int64_t>(seqs, tokens), 8);
+    w.gemv_part_bytes = size_t(kGemvMaxSplit) * r8 * rows * 4;
+    w.gemv_part = take(w.gemv_part_bytes);
+    w.gemv_ctr_count = static_cast<int>((rows + 15) / 16);
+    w.gemv_ctr = take(size_t(w.gemv_ctr_count) * 4);
+  }
   w.total = at;
   return w;
 }

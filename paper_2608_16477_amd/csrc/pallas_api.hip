@@ -320,10 +320,23 @@ const uint16_t* u16(const void* p) { return static_cast<const uint16_t*>(p); }
 
 // Projection of `rows` activation rows: the MFMA GEMM, or the skinny kernel
 // for up to 8 rows.
+// Scratch of the projections of one call: split-K partial sums of the
+// GEMM, and partial sums plus arrival counters of the skinny kernel.
+struct ProjScratch {
+  float* split;
+  size_t split_bytes;
+  float* gv_part;
+  size_t gv_part_bytes;
+  int* gv_ctr;
+  int gv_ctr_count;
+};
+
 hipError_t project(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C, int ldc,
-                   int rows, int N, int K, float* split, size_t split_bytes, hipStream_t s) {
-  if (rows <= 8) return pallas::launch_gemv(epi, A, lda, B, ldb, C, ldc, rows, N, K, s);
-  return pallas::launch_gemm(epi, A, lda, B, ldb, C, ldc, rows, N, K, split, split_bytes, s);
+                   int rows, int N, int K, const ProjScratch& sc, hipStream_t s) {
+  if (rows <= 8)
+    return pallas::launch_gemv(epi, A, lda, B, ldb, C, ldc, rows, N, K, sc.gv_part, sc.gv_part_bytes, sc.gv_ctr,
+                               sc.gv_ctr_count, s);
+  return pallas::launch_gemm(epi, A, lda, B, ldb, C, ldc, rows, N, K, sc.split, sc.split_bytes, s);
 }
 
 int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const int32_t* ids,
@@ -431,6 +444,10 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
   const int H = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int QKV = (Hq + 2 * Hkv) * d, QD = Hq * d;
 
+  const ProjScratch sc{split, sb, reinterpret_cast<float*>(ws + w.gemv_part), w.gemv_part_bytes,
+                       reinterpret_cast<int*>(ws + w.gemv_ctr), w.gemv_ctr_count};
+  if (hipError_t e = pallas::launch_zero_counters(sc.gv_ctr, sc.gv_ctr_count, s); e != hipSuccess)
+    return hip_fail(e, "counters");
   PALLAS_TRY(PALLAS_K_ROPE_TABLE, pallas::launch_rope_table(rm, B, d, c.rope_theta, rope, s), "rope table");
   PALLAS_TRY(PALLAS_K_EMBED, pallas::launch_embed_rmsnorm(tokens, u16(m->embed), u16(m->layers[0].attn_norm), r, h, B, H,
                                           c.rms_eps, c.vocab, err, s), "embed");
@@ -465,7 +482,7 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
     const pallas_layer_weights& L = m->layers[l];
     const Planes pl = layer_planes(pool, l);
     if (l > 0) PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.attn_norm), h, B, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, B, QKV, H, split, sb, s), "qkv proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiBf16, h, H, u16(L.w_qkv), H, qkv, QKV, B, QKV, H, sc, s), "qkv proj");
     qp.q_gain = u16(L.q_norm);
     qp.k_gain = u16(L.k_norm);
     qp.k_plane = pl.k;
@@ -474,13 +491,13 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
     PALLAS_TRY(PALLAS_K_DECODE_ATTN, pallas::launch_attention_decode(ap, rm, part, pallas::kDecodeMaxSplits, s), "decode attention");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, split, sb, s), "o proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, sc, s), "o proj");
     PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, B, H, c.rms_eps, s), "rmsnorm");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, split, sb, s), "gate_up proj");
-    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, B, H, F, split, sb, s), "down proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, sc, s), "gate_up proj");
+    PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, act, F, u16(L.w_down), F, r, H, B, H, F, sc, s), "down proj");
   }
   PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(m->final_norm), h, B, H, c.rms_eps, s), "final norm");
-  PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiF32, h, H, u16(m->lm_head), H, logits, c.vocab, B, c.vocab, H, split, sb, s), "lm_head");
+  PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiF32, h, H, u16(m->lm_head), H, logits, c.vocab, B, c.vocab, H, sc, s), "lm_head");
   return PALLAS_OK;
 }
 
