@@ -253,14 +253,20 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
 #pragma unroll
       for (int e = 0; e < 4; ++e) pk[e] = pack_bf2(st[t][base + 2 * e], st[t][base + 2 * e + 1]);
       const bf16x8 pb = __builtin_bit_cast(bf16x8, pk);
+      // The swizzle XORs the key with 8 dt (dt = dv / 32): 16-key block cc
+      // sits at block cc ^ (dt / 2), and with odd dt its upper 8 keys come
+      // first.  The two 8-byte halves are read in address order, and odd
+      // rows take the probabilities with their halves swapped (a sum is
+      // order-free), so no register moves precede the MFMA.
+      const bf16x8 pb_swap = __builtin_bit_cast(bf16x8, u32x4{pk[2], pk[3], pk[0], pk[1]});
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        // keys cc*16 + g*4 + {0..3} and + 8, at their swizzled slots (dv / 32 == dt)
-        const uint16_t* vrow = Vb + dt * 32 * VROW;
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + ((cc * 16) ^ (8 * dt)));
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + ((cc * 16 + 8) ^ (8 * dt)));
-        const u32x4 av = {lo.x, lo.y, hi.x, hi.y};
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pb,
+        // keys cc*16 + g*4 + {0..3} and + 8, at their swizzled slots
+        const uint16_t* vrow = Vb + dt * 32 * VROW + (cc ^ (dt >> 1)) * 16;
+        const u32x2 a0 = *reinterpret_cast<const u32x2*>(vrow);
+        const u32x2 a1 = *reinterpret_cast<const u32x2*>(vrow + 8);
+        const u32x4 av = {a0.x, a0.y, a1.x, a1.y};
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), (dt & 1) ? pb_swap : pb,
                                                            oacc[dt], 0, 0, 0);
       }
     }
