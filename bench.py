@@ -190,7 +190,10 @@ def copies_stress(P, seed):
     pages occupied, suffixes of 64-4096 tokens moved as in-order 32-token
     chunks, all chunks of one suffix in one launch.  Ten warm-up calls, then
     the median of 50 event-timed calls per figure; one more row times one
-    launch per 32-token chunk."""
+    launch per 32-token chunk.  Each row also times a plain contiguous device
+    copy of the same payload (torch's copy kernel): the practical ceiling.
+    Up to about 256 MB read + written the MI355X's 256 MB last-level cache
+    absorbs the writes; above it a plain copy runs at about 0.64 of peak."""
     import numpy as np
     import torch
     from workloads import configs, gen
@@ -234,11 +237,18 @@ def copies_stress(P, seed):
         nbytes = 2 * s * row
         t_pack = median_us(lambda: P.pallas_pack_suffix_blocks(src, src_bt, descs, arena, err))
         t_asm = median_us(lambda: P.pallas_assemble_kv(dst, dst_bt, hdrs, arena, 7, 1, err))
+        # practical ceiling: a plain contiguous device copy of the same payload
+        # (torch's copy kernel), timed the same way
+        ca = arena[: s * row]
+        cb = torch.empty_like(ca)
+        t_copy = median_us(lambda: cb.copy_(ca))
+        del cb
         rows.append({"suffix_tokens": s, "chunks_per_launch": len(descs), "bytes": nbytes,
                      "pack_us": t_pack, "pack_GBps": nbytes / t_pack / 1e3,
                      "pack_hbm_frac": nbytes / t_pack / 1e3 / PEAK_HBM_GBPS,
                      "assemble_us": t_asm, "assemble_GBps": nbytes / t_asm / 1e3,
-                     "assemble_hbm_frac": nbytes / t_asm / 1e3 / PEAK_HBM_GBPS})
+                     "assemble_hbm_frac": nbytes / t_asm / 1e3 / PEAK_HBM_GBPS,
+                     "device_copy_us": t_copy, "device_copy_hbm_frac": nbytes / t_copy / 1e3 / PEAK_HBM_GBPS})
     # one launch per 32-token chunk
     c = configs.STRESS_CHUNK
     one_d = [P.ChunkDesc(n_src - c, c, 0)]

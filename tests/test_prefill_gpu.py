@@ -72,6 +72,22 @@ def test_tiny_full_depth(P, qk_norm):
             assert np.all(raw[:, :, pg] == 0x7FA5)
 
 
+@pytest.mark.parametrize("p", [1, 15, 16, 17])
+def test_tiny_page_boundary_lengths(P, p):
+    """Prefixes of one token, and just below, at and just past one page."""
+    cfg = configs.TINY.replace(qk_norm=True)
+    glob, layers = gen.model_weights(cfg, seed=12, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    ids = gen.token_ids(p, cfg.vocab, seed=12, stream=p).numpy()
+    bt = gen.block_table(2, 8, 2, 12, p)
+    pool = run_prefill(P, model, cfg, [ids], [bt], 8)
+    check_against_oracle(cfg, glob, layers, ids, pool, bt)
+    # slots past the prefix on its pages keep their bytes
+    raw = pool.view(torch.int16).cpu().numpy()
+    for t in range(p, 32):
+        assert np.all(raw[:, :, bt[t // 16], t % 16] == 0x7FA5)
+
+
 @pytest.mark.parametrize("shape", ["mid", "large"])
 def test_layer_shapes_reduced_depth(P, shape):
     base = configs.preset(shape)
