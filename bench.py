@@ -481,12 +481,24 @@ def cpu_baseline(setup):
     from oracle import model as om
     from oracle import paged
 
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()
-                       if i.get("user_api") == "blas"] or [os.cpu_count() or 1])
+        infos = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max([i.get("num_threads", 1) for i in infos] or [os.cpu_count() or 1])
+        if infos:
+            blas = f"{infos[0].get('internal_api', '?')} {infos[0].get('version', '')}".strip()
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
     cfg = setup.cfg
     shp = om.Shape.of(cfg)
     w = {k: v.to("cpu", torch.float64).numpy() for k, v in setup.layers[0].items()}
@@ -509,6 +521,7 @@ def cpu_baseline(setup):
     del src
     return {
         "value": tok_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+        "cpu_model": cpu_model, "blas": blas, "host_cpus": os.cpu_count(),
         "sample": (f"oracle decoder layer 0 in float64 over the {p}-token prefix "
                    f"({t_layer:.2f} s), scaled by {cfg.n_layers} layers"),
         "pack_GBps": 2 * chunk.nbytes / t_pack / 1e9,
