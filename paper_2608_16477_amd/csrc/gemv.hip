@@ -75,7 +75,8 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
 #pragma unroll
     for (int t = 0; t < TILES; ++t) {
       trow[t] = (tile * TILES + t) * 16;
-      tvalid[t] = max(0, min(16, N - trow[t]));
+      // The same in every lane: keeps the descriptors in scalar registers.
+      tvalid[t] = __builtin_amdgcn_readfirstlane(max(0, min(16, N - trow[t])));
     }
   }
   auto tile_rsrc = [&](int t) {
