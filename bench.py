@@ -77,7 +77,7 @@ def parse():
                     help="skip the stress-layout copy measurements (suffixes of 64-4096 tokens)")
     ap.add_argument("--no-chunked", action="store_true",
                     help="skip the chunked-prefill measurements (256-token chunks, with 0-3 "
-                         "resident decode sessions interleaved)")
+                         "resident decode sessions interleaved) and the post-handover recompute legs")
     ap.add_argument("--no-staging", action="store_true",
                     help="skip the pinned-host staging legs and the two-stream overlap measurement")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -339,6 +339,57 @@ def chunked_prefill(st, chunk=256, residents=(0, 1, 2, 3), reps=3, resident_ctx=
     out["kernels_ms"] = {k: v[0] for k, v in prof.items() if v[1]}
     torch.cuda.synchronize()
     assert int(err.item()) == 0, "device-side error flag raised in the chunked prefill"
+    return out
+
+
+def post_handover_recompute(st, assemble_ms, reps=3, chunk=256):
+    """What the target pays after handover when a suffix is recomputed
+    instead of migrated (the "w/o SM" variant of the ablation study, Sec.
+    6.5), and when the whole history is (the recomputation baseline): the
+    first request's suffix [p, n) prefilled over its prefix K/V already in
+    the target pool (pallas_prefill_chunk, as one call and in `chunk`-token
+    chunks), and a prefill of all n tokens.  Median of `reps` runs after
+    one warm-up, against assembling the migrated suffix (`assemble_ms`)."""
+    import numpy as np
+    import torch
+
+    model, stream = st.model, torch.cuda.current_stream()
+    n, p = st.ns[0], st.ps[0]
+    ids = torch.tensor(st.ids[0][:n], dtype=torch.int32, device="cuda")
+    bt = st.dst_tab[:1]
+
+    def suffix_one():
+        model.prefill_chunk(ids[p:n], [0, n - p], [p], bt, st.dst, st.ws, st.err)
+
+    def suffix_chunks():
+        for a in range(p, n, chunk):
+            b = min(a + chunk, n)
+            model.prefill_chunk(ids[a:b], [0, b - a], [a], bt, st.dst, st.ws, st.err)
+
+    def history():
+        model.prefill_prefix(ids, [0, n], bt, st.dst, st.ws, st.err)
+
+    def median_ms(fn):
+        fn()
+        times = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        return float(np.median(times))
+
+    out = {"prefix_tokens": p, "suffix_tokens": n - p, "assemble_ms": assemble_ms}
+    for name, fn, tokens in (("suffix_one_call", suffix_one, n - p),
+                             (f"suffix_chunks_{chunk}", suffix_chunks, n - p),
+                             ("whole_history", history, n)):
+        ms = median_ms(fn)
+        out[name] = {"ms": ms, "tokens_per_s": tokens / ms * 1e3,
+                     "vs_assemble": ms / assemble_ms if assemble_ms > 0 else None}
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0, "device-side error flag raised in the recompute legs"
     return out
 
 
@@ -681,6 +732,8 @@ def main():
         print("[bench] chunked prefill", file=sys.stderr, flush=True)
         out["chunked_prefill"] = chunked_prefill(st)
         out["chunked_prefill"]["whole_prefix_ms"] = phase_ms["prefill"]
+        print("[bench] post-handover recompute", file=sys.stderr, flush=True)
+        out["post_handover_recompute"] = post_handover_recompute(st, phase_ms["assemble"])
     out["scheduler"] = scheduler_decision(P, cfg, st.ps[0] if wl.num_seqs == 1 else prefix_tokens,
                                           phase_ms["prefill"], phase_ms["assemble"], phase_ms["decode"])
     if not args.no_staging:
