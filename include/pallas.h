@@ -173,7 +173,9 @@ size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t 
  * with bt_i = d_block_tables + i * max_pages (int32, device).  Nothing else
  * is written to the pool; no logits are produced.  num_seqs in
  * [1, PALLAS_MAX_SEQS]; 1 <= p_i <= PALLAS_MAX_PREFILL_LEN (UNSUPPORTED
- * beyond); sum p_i <= the workspace's max_tokens.
+ * beyond); sum p_i <= the workspace's max_tokens.  One layer's K plane of
+ * the pool (num_pages * page * n_kv_heads * head_dim * 2 bytes) must not
+ * exceed 4 GiB (UNSUPPORTED): attention addresses it with 32-bit offsets.
  * Table entries outside [0, num_pages) are skipped and raise
  * PALLAS_DEVERR_PAGE in *d_err (nullable, device, caller clears it). */
 int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
@@ -195,7 +197,7 @@ int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_to
  * gives the same cache, up to rounding, as one prefill over the whole
  * prefix.  Limits: s_i + p_i <= max_pages * page (OUT_OF_RANGE) and
  * <= PALLAS_MAX_PREFILL_LEN (UNSUPPORTED); sum p_i <= the workspace's
- * max_tokens.  Slots [0, s_i) are read, never checked: the caller must
+ * max_tokens; the 4 GiB K-plane limit of pallas_prefill_prefix.  Slots [0, s_i) are read, never checked: the caller must
  * have filled them. */
 int pallas_prefill_chunk(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
                          const int32_t* h_cu_seqlens, const int32_t* h_start_pos,

@@ -1,9 +1,16 @@
 // Causal grouped-query attention over the paged KV cache.
 //
-// Prefill: one workgroup per (sequence, 32-query block, KV head) with one
-// wave per query head of the group, so each 64-key K/V tile is read from the
-// pool once for all G query heads.  The score tile is computed transposed,
-// S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: a lane then owns one query and
+// Prefill: one workgroup per (sequence, 32-query block, G query heads of one
+// KV head) with one wave per query head, so each 64-key K/V tile is read
+// from the pool once for the G heads.  G is the GQA group, except that a
+// group of 8 at head_dim 128 is split over two 4-wave workgroups, two of
+// which fit on a CU (255 registers, 75 KB of LDS each): the waves sharing a
+// SIMD then come from different workgroups and do not meet at the same
+// barriers.  K tiles go from memory straight into LDS (buffer_load ... lds);
+// V tiles are staged through registers and written transposed.
+//
+// The score tile is computed transposed, S^T = K Q^T, with
+// v_mfma_f32_32x32x16_bf16: a lane then owns one query and
 // 16 of its keys per 32-key block, so the online-softmax max and sum are
 // register reductions plus one cross-half lane swap, and the rescale of the
 // output accumulator is lane-uniform.  O^T = V^T P^T reuses the score
@@ -18,6 +25,7 @@
 // Decode: split over keys (64 per workgroup, all query heads of one KV
 // head per workgroup), then a combine pass over the splits.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -32,6 +40,8 @@ constexpr int VPAD = 4; // Vt row padding (elements): 136-byte rows spread banks
 constexpr int kPage = 16;     // tokens per cache page (the only page size the library accepts)
 constexpr int KSTR = KB + 1;  // K tile chunk stride, in 16-byte slots
 constexpr float kLazyLog2 = 8.f;  // lazy-rescale headroom, log2 units
+
+typedef __attribute__((address_space(3))) void lds_void;
 
 struct AttnSched {
   int32_t total;
@@ -56,7 +66,7 @@ __device__ __forceinline__ float xhalf_sum(float x) {
 // attn_prefill_combine_kernel merges them.  Used when a call has too few
 // query blocks to fill the chip (a 256-token chunk over a long prefix).
 template <int D, int G, bool kSplit>
-__global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowMap rm, AttnSched sch,
+__global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(AttnParams p, RowMap rm, AttnSched sch,
                                                               float* __restrict__ part) {
   constexpr int CH = D / 8;                   // 16-byte chunks per K/V row
   constexpr int ITEMS = (KB / 2) * CH;        // (key pair, chunk) staging items per tile
@@ -66,14 +76,19 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
   // K tile as [chunk][key] with a chunk stride of KB + 1 slots: the score
   // MFMA reads 32 consecutive keys of one chunk, and the staging writes of
   // 16 chunks of one key pair land in distinct banks.
-  __shared__ __attribute__((aligned(16))) u32x4 Ks[2][CH * KSTR];
+  // Two K buffers as separate arrays, chosen by a compile-time parity, so
+  // the compiler can tell a tile loading into one from reads of the other.
+  __shared__ __attribute__((aligned(16))) u32x4 Ks0[CH * KSTR];
+  __shared__ __attribute__((aligned(16))) u32x4 Ks1[CH * KSTR];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VROW];
   __shared__ int32_t bts[kMaxPrefillLen / kPage];   // the sequence's block-table entries
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int g = lane >> 5, l32 = lane & 31;
-  const int kh = blockIdx.y;
-  const int h = kh * G + wave;
+  // Workgroup y covers query heads [y G, y G + G), all of one KV head (G
+  // divides the group size Hq / Hkv).
+  const int h = static_cast<int>(blockIdx.y) * G + wave;
+  const int kh = __builtin_amdgcn_readfirstlane(h / (p.Hq / p.Hkv));
 
   const int gidx = sch.total - 1 - static_cast<int>(blockIdx.x);  // longest blocks first
   int s = 0;
@@ -145,8 +160,46 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
     off0 = (static_cast<int64_t>(pg) * kPage + (pc & (kPage - 1))) * row_stride;
     off1 = off0 + (pos + 1 < kend ? row_stride : 0);
   };
-  // Staging registers: each thread owns MAXIT (key pair, chunk) items.
-  u32x4 skr[MAXIT][2], svr[MAXIT][2];
+  // V staging registers: each thread owns MAXIT (key pair, chunk) items.
+  u32x4 svr[MAXIT][2];
+  // V loads this wave issues per tile (threads past the last item issue
+  // none; wave-uniform).
+  int nvload = 0;
+#pragma unroll
+  for (int r = 0; r < MAXIT; ++r)
+    if (wave * 64 + r * nthreads < ITEMS) nvload += 2;
+  // K tile straight from memory into LDS: instruction c (16-byte chunk c of
+  // the head dimension) has lane l load key k0 + l, so its 64 lanes fill
+  // the 64 consecutive slots of chunk c.  Each wave issues CH / G of them.
+  // The K plane is addressed through a buffer descriptor with 32-bit
+  // offsets (the host keeps a plane under 4 GiB).
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)kbase, 0, static_cast<uint32_t>(p.plane_bytes - static_cast<int64_t>(kh) * D * 2), 0x00020000);
+  auto dmaK = [&](u32x4* Kd, int k0) {
+    const int pc = min(k0 + lane, kend - 1);
+    int pg = bts[pc >> 4];
+    pg = (pg >= 0 && pg < p.num_pages) ? pg : 0;
+    const uint32_t off = static_cast<uint32_t>((pg * kPage + (pc & (kPage - 1))) * row_stride * 2);
+#pragma unroll
+    for (int i = 0; i < CH / G; ++i) {
+      const int ch = wave * (CH / G) + i;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(Kd + ch * KSTR), 16, off + ch * 16, 0, 0, 0);
+    }
+  };
+  // Wait until at most n of this wave's memory loads are outstanding.
+  auto wait_vm = [](int n) {
+    switch (n) {
+      case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+      case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+      case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+      case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+      case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+      case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+      case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+      case 14: asm volatile("s_waitcnt vmcnt(14)" ::: "memory"); break;
+      default: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    }
+  };
   auto gload = [&](u32x4 (&dst)[MAXIT][2], const uint16_t* base, int k0) {
 #pragma unroll
     for (int r = 0; r < MAXIT; ++r) {
@@ -157,16 +210,6 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
       pair_off(k0 + 2 * kp, o0, o1);
       dst[r][0] = *reinterpret_cast<const u32x4*>(base + o0 + ch * 8);
       dst[r][1] = *reinterpret_cast<const u32x4*>(base + o1 + ch * 8);
-    }
-  };
-  auto swriteK = [&](int buf) {
-#pragma unroll
-    for (int r = 0; r < MAXIT; ++r) {
-      const int it = threadIdx.x + r * nthreads;
-      if (ITEMS % nthreads != 0 && it >= ITEMS) break;
-      const int ch = it % CH, kp = it / CH;
-#pragma unroll
-      for (int e = 0; e < 2; ++e) Ks[buf][ch * KSTR + 2 * kp + e] = skr[r][e];
     }
   };
   auto swriteV = [&](int buf) {
@@ -188,8 +231,8 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
   auto barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
   // S^T = K Q^T for one 64-key tile: keys t*32 + [0,32) in st[t].
-  auto scores = [&](int buf, f32x16 (&st)[2]) {
-    const u32x4* Kb = Ks[buf] + g * KSTR + l32;
+  auto scores = [&](const u32x4* Ksrc, f32x16 (&st)[2]) {
+    const u32x4* Kb = Ksrc + g * KSTR + l32;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
@@ -277,40 +320,42 @@ __global__ __launch_bounds__(G * 64) void attn_prefill_kernel(AttnParams p, RowM
   };
 
   // Pipeline: while tile j's softmax runs, tile j+1's scores are computed
-  // from its K tile (already in LDS); K is staged two tiles ahead, V one.
-  gload(skr, kbase, kt0);
+  // from its K tile (already in LDS).  K tiles go straight to LDS two tiles
+  // ahead; V tiles are loaded into registers one tile ahead and written
+  // transposed.
+  dmaK(Ks0, kt0);
+  if (ntiles > 1) dmaK(Ks1, kt0 + KB);
   gload(svr, vbase, kt0);
-  swriteK(0);
   swriteV(0);
-  if (ntiles > 1) {
-    gload(skr, kbase, kt0 + KB);
-    swriteK(1);
-    gload(svr, vbase, kt0 + KB);
-  }
-  if (ntiles > 2) gload(skr, kbase, kt0 + 2 * KB);
+  if (ntiles > 1) gload(svr, vbase, kt0 + KB);
+  wait_vm(ntiles > 1 ? nvload : 0);   // K_0 and K_1 have landed
   barrier();
   // One pipeline step: scores of tile j+1 into `nxt` while tile j (scores in
-  // `cur`, wholly below the diagonal) goes through softmax and PV.
-  auto step = [&](int j, f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+  // `cur`, wholly below the diagonal) goes through softmax and PV.  B = j % 2
+  // is a template constant: K_j sat in buffer B, K_{j+1} sits in 1 - B.
+  auto step = [&](auto parity, int j, f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
+    constexpr int B = decltype(parity)::value;
+    u32x4* Kfree = B == 0 ? Ks0 : Ks1;
+    const u32x4* Knext = B == 0 ? Ks1 : Ks0;
     barrier();   // K_{j+1} and V_j resident; the buffers of K_j and V_{j-1} free
-    scores((j + 1) & 1, nxt);
+    if (j + 2 < ntiles) dmaK(Kfree, kt0 + (j + 2) * KB);
+    scores(Knext, nxt);
     float alpha;
     if (softmax(cur, alpha)) rescale(alpha);
-    pv(j & 1, cur);
-    if (j + 2 < ntiles) swriteK(j & 1);
-    swriteV((j + 1) & 1);
-    if (j + 3 < ntiles) gload(skr, kbase, kt0 + (j + 3) * KB);
+    pv(B, cur);
+    swriteV(1 - B);
     if (j + 2 < ntiles) gload(svr, vbase, kt0 + (j + 2) * KB);
+    wait_vm(j + 2 < ntiles ? nvload : 0);   // K_{j+2} lands before the next barrier
   };
   f32x16 sa[2], sb[2];
-  scores(0, sa);
+  scores(Ks0, sa);
   int j = 0;
   for (; j + 2 < ntiles; j += 2) {
-    step(j, sa, sb);
-    step(j + 1, sb, sa);
+    step(std::integral_constant<int, 0>{}, j, sa, sb);
+    step(std::integral_constant<int, 1>{}, j + 1, sb, sa);
   }
   if (j + 1 < ntiles) {
-    step(j, sa, sb);
+    step(std::integral_constant<int, 0>{}, j, sa, sb);
 #pragma unroll
     for (int t = 0; t < 2; ++t) sa[t] = sb[t];
   }
@@ -532,7 +577,7 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
     for (int key = 0; key < jn; ++key) {
       const float pw = sc[g][key];
       const uint16_t* vr = &Vs[key * KROW + dv0];
-      if (OPT == 4) {
+      if constexpr (OPT == 4) {
         const u32x2 v = *reinterpret_cast<const u32x2*>(vr);
         o[0] += pw * bflo(v.x);
         o[1] += pw * bfhi(v.x);
@@ -609,14 +654,18 @@ hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, float
   }
   sch.total = sch.prefix[rm.n_seqs];
   if (sch.total == 0) return hipSuccess;
-  const int G = p.Hq / p.Hkv;
+  // Query heads per workgroup: the whole GQA group, except that a group of
+  // 8 at head_dim 128 is split over two 4-wave workgroups, two of which fit
+  // on a CU, so the waves sharing a SIMD do not share barriers.
+  const int group = p.Hq / p.Hkv;
+  const int G = (group == 8 && p.d == 128) ? 4 : group;
   if (maxlen > kMaxPrefillLen || p.page != kPage) return hipErrorInvalidValue;
   const int rows = rm.cu[rm.n_seqs];
-  const int S = attn_prefill_splits(rows, sch.total * p.Hkv, (maxlen + KB - 1) / KB);
+  const int S = attn_prefill_splits(rows, sch.total * (p.Hq / G), (maxlen + KB - 1) / KB);
   sch.split_tiles = (((maxlen + KB - 1) / KB) + S - 1) / S;
   if (S > 1 && (!part || part_bytes < attn_prefill_split_bytes(rows, p.Hq, p.d)))
     return hipErrorInvalidValue;
-  dim3 grid(sch.total, p.Hkv, S);
+  dim3 grid(sch.total, p.Hq / G, S);
 #define PALLAS_ATTN_CASE(DD, GG)                                                                 \
   if (p.d == DD && G == GG) {                                                                    \
     if (S == 1) {                                                                                \

@@ -159,6 +159,7 @@ struct AttnParams {
   const uint16_t* v_plane;
   const int32_t* bt;
   int max_pages, num_pages, page;
+  int64_t plane_bytes;     // bytes of one K (or V) plane: num_pages * page * Hkv * d * 2
   uint16_t* o;             // [rows][Hq * d]
   int Hq, Hkv, d;
   float scale_log2;        // log2(e) / sqrt(d)

@@ -377,6 +377,7 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
   ap.bt = bt;
   ap.max_pages = max_pages;
   ap.num_pages = pool->num_pages;
+  ap.plane_bytes = int64_t(pool->num_pages) * pool->page_size * pool->n_kv_heads * pool->head_dim * 2;
   ap.page = pool->page_size;
   ap.o = o;
   ap.Hq = Hq;
@@ -472,6 +473,7 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
   ap.bt = bt;
   ap.max_pages = max_pages;
   ap.num_pages = pool->num_pages;
+  ap.plane_bytes = int64_t(pool->num_pages) * pool->page_size * pool->n_kv_heads * pool->head_dim * 2;
   ap.page = pool->page_size;
   ap.o = o;
   ap.Hq = Hq;
@@ -527,6 +529,10 @@ int prefill_call(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
   if (!d_token_ids || !h_cu_seqlens || !d_block_tables || max_pages <= 0)
     return fail(PALLAS_ERR_INVALID_ARG, "%s: null ids, cu_seqlens or block tables", what);
   if (int rc = check_model_pool(m, pool, what)) return rc;
+  // Prefill attention loads K tiles through 32-bit offsets into a layer's K plane.
+  const int64_t plane = int64_t(pool->num_pages) * pool->page_size * pool->n_kv_heads * pool->head_dim * 2;
+  if (plane > int64_t(0xFFFFFFFFll))
+    return fail(PALLAS_ERR_UNSUPPORTED, "%s: a layer's K plane of %lld bytes exceeds 4 GiB", what, (long long)plane);
   pallas::RowMap rm;
   rm.n_seqs = num_seqs;
   if (h_cu_seqlens[0] != 0) return fail(PALLAS_ERR_INVALID_ARG, "%s: cu_seqlens[0] must be 0", what);
