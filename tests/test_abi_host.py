@@ -162,6 +162,46 @@ def test_prefill_rejects_sequences_beyond_the_length_limit(P):
         h.pallas_model_destroy(model)
 
 
+def test_prefill_rejects_k_planes_beyond_4_gib(P):
+    """Prefill attention addresses one layer's K plane with 32-bit offsets:
+    a pool whose plane (num_pages * page * n_kv_heads * head_dim * 2 bytes)
+    exceeds 4 GiB - 1 is refused on the host (UNSUPPORTED) before anything
+    touches the device; one page fewer passes that check and stops at the
+    (undersized) workspace instead.  Both prefill calls apply it."""
+    from workloads import configs
+    from paper_2608_16477_amd.binding import ModelConfigC, WeightsC, LayerWeightsC, KVPoolC
+    h = P.lib()
+    c = configs.TINY
+    cc = ModelConfigC(c.n_layers, c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn,
+                      c.vocab, c.rms_eps, c.rope_theta, int(c.qk_norm), c.page_size)
+    la = (LayerWeightsC * c.n_layers)()
+    for l in range(c.n_layers):
+        for name, _ in LayerWeightsC._fields_:
+            setattr(la[l], name, FAKE)
+    w = WeightsC(FAKE, FAKE, FAKE, la)
+    model = C.c_void_p()
+    assert h.pallas_model_create(C.byref(cc), C.byref(w), C.byref(model)) == 0
+    page_bytes = c.page_size * c.n_kv_heads * c.head_dim * 2
+    first_refused = (1 << 32) // page_bytes          # plane of exactly 4 GiB
+    assert (first_refused * page_bytes) == 1 << 32
+    try:
+        def rc(pages, chunk):
+            pool = KVPoolC(FAKE, pages, c.page_size, c.n_layers, c.n_kv_heads, c.head_dim)
+            cu = (C.c_int32 * 2)(0, 16)
+            if chunk:
+                start = (C.c_int32 * 1)(16)
+                return P.Status(h.pallas_prefill_chunk(model, 1, FAKE, cu, start, FAKE, 4, C.byref(pool),
+                                                       FAKE, 256, None, None))
+            return P.Status(h.pallas_prefill_prefix(model, 1, FAKE, cu, FAKE, 4, C.byref(pool),
+                                                    FAKE, 256, None, None))
+        for chunk in (False, True):
+            assert rc(first_refused, chunk) == P.Status.UNSUPPORTED
+            assert "4 GiB" in P.pallas_last_error()
+            assert rc(first_refused - 1, chunk) == P.Status.WORKSPACE
+    finally:
+        h.pallas_model_destroy(model)
+
+
 def test_profile_clock_arguments(P):
     """The clock query rejects a class outside the enumeration; with nothing
     sampled it reports 0 GHz and 0 workgroups."""
