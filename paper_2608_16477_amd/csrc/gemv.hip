@@ -9,7 +9,10 @@
 // stage the 16-byte slots are permuted so the v_mfma_f32_16x16x32_bf16
 // operand reads (16 rows at one k) hit 16 distinct bank groups.  The four
 // partial tiles are summed through LDS and the epilogue matches the prefill
-// GEMM's.
+// GEMM's.  Launches with fewer than two tiles per CU (O and down) also split
+// K over up to kGemvMaxSplit workgroups per tile: each writes its partial
+// sums with agent-scope stores and counts itself in a per-tile counter, and
+// the last to arrive adds the splits in order and applies the epilogue.
 #include <cmath>
 
 #include "common.h"
