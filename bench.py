@@ -79,7 +79,8 @@ def parse():
                     help="skip the chunked-prefill measurements (256-token chunks, with 0-3 "
                          "resident decode sessions interleaved) and the post-handover recompute legs")
     ap.add_argument("--no-staging", action="store_true",
-                    help="skip the pinned-host staging legs and the two-stream overlap measurement")
+                    help="skip the pinned-host staging legs and the two-stream overlap measurements "
+                         "(back to back and paced at 100-500 Mbps)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 1 GiB device-to-device copy and exit (the reference "
                          "point for scaling FETCH_SIZE / WRITE_SIZE counter readings)")
@@ -500,6 +501,85 @@ def overlapped_preparation(st, chunk=32, reps=3):
     return out
 
 
+def paced_preparation(st, rates_mbps=(100, 300, 500), chunk=32, prefills=6):
+    """Overlapped preparation with the suffix arriving at network rates
+    (the evaluation's links run at 100-500 Mbps): `prefills` back-to-back
+    prefix prefills are enqueued on one stream (from a host thread), while
+    the main thread releases one `chunk`-token chunk assembly on another
+    stream each time a chunk's payload would have crossed a link of the
+    given rate (payload bits / rate), until the prefills finish.  Reports,
+    per rate, the chunks released, the median prefill time against the
+    prefills alone, and the chunk assemblies' times (events around each
+    launch on its stream: waiting for CU slots plus copying)."""
+    import threading
+    import numpy as np
+    import torch
+
+    P, cfg = st.P, st.cfg
+    n, p = st.ns[0], st.ps[0]
+    hdrs = [P.ChunkHeader(1000, 1, t, min(chunk, n - t), (t - p) * st.row_bytes, cfg.n_layers,
+                          cfg.n_kv_heads, cfg.head_dim, 2) for t in range(p, n, chunk)]
+    P.pallas_pack_suffix_blocks(st.src, st.src_tab[0], [P.ChunkDesc(h.start_pos, h.num_tokens, h.arena_offset)
+                                                        for h in hdrs], st.arena, st.err)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    chunk_bits = chunk * st.row_bytes * 8
+
+    def run(rate):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(prefills)]
+        done = torch.cuda.Event()
+        torch.cuda.synchronize()
+
+        def enqueue():
+            for a, b in evs:
+                a.record(sa)
+                st.model.prefill_prefix(st.prefix_ids[:p], [0, p], st.dst_tab[:1], st.dst, st.ws, st.err,
+                                        stream=sa)
+                b.record(sa)
+            done.record(sa)
+
+        th = threading.Thread(target=enqueue)
+        t0 = time.perf_counter()
+        th.start()
+        asm = []
+        if rate:
+            interval = chunk_bits / (rate * 1e6)
+            k = 0
+            while True:
+                target = t0 + (k + 1) * interval
+                now = time.perf_counter()
+                if now < target:
+                    time.sleep(target - now)
+                if not th.is_alive() and done.query():
+                    break
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(sb)
+                P.pallas_assemble_kv(st.dst, st.dst_tab[0], [hdrs[k % len(hdrs)]], st.arena, 1000, 1, st.err,
+                                     stream=sb)
+                e1.record(sb)
+                asm.append((e0, e1))
+                k += 1
+        th.join()
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs], [a.elapsed_time(b) * 1e3 for a, b in asm]
+
+    run(None)
+    alone, _ = run(None)
+    out = {"chunk_tokens": chunk, "chunk_bytes": chunk * st.row_bytes, "prefills": prefills,
+           "prefill_alone_ms": float(np.median(alone)), "rows": []}
+    for rate in rates_mbps:
+        pre, asm = run(rate)
+        row = {"rate_mbps": rate, "chunk_interval_ms": chunk_bits / (rate * 1e6) * 1e3,
+               "chunks_released": len(asm), "prefill_ms": float(np.median(pre)),
+               "prefill_slowdown": float(np.median(pre)) / out["prefill_alone_ms"]}
+        if asm:
+            row["assemble_us_median"] = float(np.median(asm))
+            row["assemble_us_max"] = float(np.max(asm))
+        out["rows"].append(row)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    return out
+
+
 def scheduler_decision(P, cfg, prefix_tokens, prefill_ms, assemble_ms, decode_ms, calls=20000):
     """The Scheduler Engine fed with this run's measurements: r_p = the
     measured prefix-prefill rate, r_d = one token per measured decode step,
@@ -740,6 +820,7 @@ def main():
         print("[bench] wire staging and overlapped preparation", file=sys.stderr, flush=True)
         out["wire_staging"] = wire_staging(st)
         out["overlapped_preparation"] = overlapped_preparation(st)
+        out["paced_preparation"] = paced_preparation(st)
     if not args.no_stress:
         print("[bench] stress-layout copies", file=sys.stderr, flush=True)
         out["copies_stress"] = copies_stress(P, args.seed)
