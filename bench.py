@@ -597,7 +597,14 @@ def scheduler_decision(P, cfg, prefix_tokens, prefill_ms, assemble_ms, decode_ms
     for _ in range(calls):
         P.pallas_window_select(k_curr, t_remain, **params)
     us = (time.perf_counter() - t0) / calls * 1e6
-    return {"inputs": {**params, "k_curr": k_curr, "t_remain": t_remain},
+    # The trade-off behind the choice (the shape of the paper's window
+    # figures): the model's terms at windows from 0 to T_max.
+    curve = []
+    for t_w in sorted({0.0, 0.05, 0.1, 0.3, 0.5, 1.0, 2.0, 3.0, params["t_max"], d.t_w}):
+        e = P.pallas_window_evaluate(k_curr, t_remain, t_w, **params)
+        curve.append({"t_w": t_w, "cost": e.cost, "t_sit_s": e.t_sit, "t_early_s": e.t_early,
+                      "t_hist_s": e.t_hist, "t_res_s": e.t_res, "l_hist": e.l_hist})
+    return {"inputs": {**params, "k_curr": k_curr, "t_remain": t_remain}, "curve": curve,
             "t_w": d.t_w, "t_sit_s": d.t_sit, "t_early_s": d.t_early, "t_hist_s": d.t_hist,
             "t_res_s": d.t_res, "trigger": bool(d.trigger), "candidates": d.n_candidates,
             "decision_us": us}
