@@ -25,7 +25,13 @@
  *   - Device pointers are named d_*, host pointers h_*.  All device memory
  *     (weights, pools, tables, chunk arenas, logits, workspace) belongs to the
  *     caller; the library allocates no device memory and keeps no pointer
- *     beyond a call, except the weight pointers kept by a model handle.
+ *     beyond a call, except the weight pointers kept by a model handle (and
+ *     the opt-in profiling calls, which allocate a 312-byte counter array
+ *     once per process).
+ *   - Calls may come from several host threads at once.  A model handle is
+ *     read-only after creation and may be shared; a workspace may not be
+ *     used by two calls whose work is in flight at the same time unless
+ *     they are ordered on one stream.
  *   - Host structs and arrays are read during the call only.
  *   - `stream` is a hipStream_t (NULL: the default stream).  Work is enqueued
  *     on it; calls return before the work completes and never synchronise.
@@ -354,7 +360,10 @@ typedef enum {
 
 /* Enable timing for the classes whose bit (1 << class) is set in
  * class_mask (0 disables).  Each timed launch is bracketed by two HIP events
- * recorded on the launch's stream; nothing else changes.  Process-wide. */
+ * recorded on the launch's stream; nothing else changes.  Process-wide and
+ * serialised by a lock.  The first nonzero mask allocates the clock
+ * counters (3 x PALLAS_K_COUNT uint64, kept until the process ends) on the
+ * device current at that call; clock sampling covers launches on it. */
 void pallas_profile_enable(uint32_t class_mask);
 
 /* Wait for every recorded event pair, add its elapsed time to the class
