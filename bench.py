@@ -613,7 +613,8 @@ def scheduler_decision(P, cfg, prefix_tokens, prefill_ms, assemble_ms, decode_ms
 def cpu_baseline(setup):
     """The oracle's first decoder layer (float64 numpy) over the workload's
     prefix rows, scaled by the layer count; plus the oracle's pack of the
-    suffix from a host copy of the source pool."""
+    suffix from a host copy of the source pool and its assembly into a host
+    copy of the target pool (GB/s = read + write of the payload)."""
     import numpy as np
     import torch
     from oracle import model as om
@@ -657,6 +658,14 @@ def cpu_baseline(setup):
     chunk = paged.pack(src, bt, p, n - p)
     t_pack = time.perf_counter() - t0
     del src
+    # assembly of that chunk into a host copy of the target pool
+    dst = setup.dst.view(torch.int16).cpu().numpy()
+    dbt = setup.dst_tab[i0].cpu().numpy()
+    hdr = paged.ChunkHeader(1, 1, p, n - p, cfg.n_layers, cfg.n_kv_heads, cfg.head_dim, 2)
+    t0 = time.perf_counter()
+    paged.assemble(dst, dbt, [hdr], [chunk], 1, 1)
+    t_asm = time.perf_counter() - t0
+    del dst
     return {
         "value": tok_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
         "cpu_model": cpu_model, "blas": blas, "host_cpus": os.cpu_count(),
@@ -664,6 +673,8 @@ def cpu_baseline(setup):
                    f"({t_layer:.2f} s), scaled by {cfg.n_layers} layers"),
         "pack_GBps": 2 * chunk.nbytes / t_pack / 1e9,
         "pack_sample": f"oracle pack of the {n - p}-token suffix ({chunk.nbytes / 1e6:.0f} MB) on 1 thread",
+        "assemble_GBps": 2 * chunk.nbytes / t_asm / 1e9,
+        "assemble_sample": f"oracle assembly of that chunk into a host copy of the target pool on 1 thread",
     }
 
 
