@@ -72,6 +72,8 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
   constexpr int VROW = KB + VPAD;
   constexpr int nthreads = G * 64;
   constexpr int MAXIT = (ITEMS + nthreads - 1) / nthreads;
+  static_assert(2 * MAXIT <= 16, "wait_vm covers at most 16 outstanding V loads per wave");
+  static_assert(CH % G == 0, "each wave issues CH / G of a K tile's chunk loads");
   // K tile as [chunk][key] with a chunk stride of KB + 1 slots: the score
   // MFMA reads 32 consecutive keys of one chunk, and the staging writes of
   // 16 chunks of one key pair land in distinct banks.
