@@ -125,6 +125,33 @@ def test_short_chunks_over_long_prefix(P):
             assert rel_err(a[l, kv], b[l, kv]) <= TOL
 
 
+def test_large_layer_shape_short_chunks(P):
+    """The large model's layer shape (8 query heads per KV head, head_dim
+    128): calls with few query blocks split each GQA group over two 4-wave
+    workgroups, and chunks of at most 256 rows also split the keys of each
+    block over several workgroups.  A 300-row first chunk (split groups, no
+    key splits), then 200-, 1- and 59-row chunks over it (split groups and
+    key splits), against the oracle and against one undivided prefill."""
+    cfg = configs.LARGE.replace(n_layers=2, vocab=4096, name="large-L2")
+    glob, layers = gen.model_weights(cfg, seed=10, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    n = 560
+    ids = gen.token_ids(n, cfg.vocab, seed=10).numpy()
+    bt = gen.block_table(35, 40, 35, 10, 2)
+    pool = empty_pool(cfg, 40, fill_bits=0x7FA5)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    chunked(model, cfg, ids, [(0, 300), (300, 500), (500, 501), (501, n)], bt, pool, err)
+    whole = empty_pool(cfg, 40, fill_bits=0x7FA5)
+    chunked(model, cfg, ids, [(0, n)], bt, whole, err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    check(cfg, glob, layers, ids, pool, bt, drift_bound=True)
+    a, b = kv_logical(pool, bt, n)[:, :, 300:], kv_logical(whole, bt, n)[:, :, 300:]
+    for l in range(cfg.n_layers):
+        for kv in (0, 1):
+            assert rel_err(a[l, kv], b[l, kv]) <= TOL
+
+
 def test_several_sequences_at_different_starts(P):
     """One call prefills the second parts of three sequences whose first
     parts an earlier call wrote."""
