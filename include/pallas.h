@@ -64,7 +64,7 @@ typedef enum {
   PALLAS_ERR_COVERAGE = 3,     /* gap or two claims on one position */
   PALLAS_ERR_STALE_EPOCH = 4,  /* chunk of another migration epoch */
   PALLAS_ERR_WRONG_REQUEST = 5,/* chunk of another request */
-  PALLAS_ERR_UNSUPPORTED = 6,  /* shape this build has no kernel for */
+  PALLAS_ERR_UNSUPPORTED = 6,  /* shape the library has no kernel for */
   PALLAS_ERR_HIP = 7,          /* a HIP runtime call failed */
   PALLAS_ERR_WORKSPACE = 8     /* workspace too small */
 } pallas_status;
