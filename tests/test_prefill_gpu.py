@@ -6,7 +6,9 @@ Shapes: the 2-layer tiny decoder (full depth; QK-norm off and on); the mid
 and large decoders' layer shapes at reduced depth and a 300-token prefix
 (several 256-row GEMM tiles, a ragged tail, ten 32-query attention blocks);
 several sequences of different lengths in one call; the causality property
-(prefix K/V bitwise equal to the first rows of a longer prefill)."""
+(prefix K/V bitwise equal to the first rows of a longer prefill); one
+sequence at the 32768-position limit (all of layer 0 and sampled rows of
+layer 1 against the oracle)."""
 import numpy as np
 import pytest
 import torch
@@ -130,6 +132,44 @@ def test_causality_and_determinism(P):
     b = kv_logical(pre, bt, p)
     np.testing.assert_array_equal(a, b)
     assert torch.equal(pre.view(torch.int16), pre2.view(torch.int16))
+
+
+def test_prefill_at_the_length_limit(P):
+    """One sequence of PALLAS_MAX_PREFILL_LEN (32768) positions, the tiny
+    decoder with QK-norm.  Layer 0's K/V depend on each token alone, so the
+    oracle gives all 32768 rows; layer 1's K/V at sampled positions t (the
+    first, page edges, the middle, the last) need one layer-0 attention row
+    over the oracle's own layer-0 K/V of [0, t].  The first 300 rows also
+    equal, bit for bit, those of a 300-token prefill."""
+    cfg = configs.TINY.replace(qk_norm=True)
+    glob, layers = gen.model_weights(cfg, seed=12, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    n = 32768
+    pages = n // 16
+    ids = gen.token_ids(n, cfg.vocab, seed=12).numpy()
+    bt = gen.block_table(pages, pages + 8, pages, 12, 1)
+    pool = run_prefill(P, model, cfg, [ids], [bt], pages + 8)
+    short = run_prefill(P, model, cfg, [ids[:300]], [bt], pages + 8)
+    lv = kv_logical(pool, bt, n)
+    np.testing.assert_array_equal(lv[:, :, :300], kv_logical(short, bt, 300))
+
+    g, ls = oracle_weights(glob, layers)
+    shp = shape_of(cfg)
+    r = om.embed(list(ids), g)
+    pos = np.arange(n)
+    _, k0, v0 = om.layer(r, pos, None, None, ls[0], shp, om.bf16_round, kv_only=True)
+    assert rel_err(lv[0, 0], k0) <= TOL
+    assert rel_err(lv[0, 1], v0) <= TOL
+    ts = [0, 1, 15, 16, 4095, 16384, 32735, 32767]
+    k1, v1 = [], []
+    for t in ts:
+        r1, _, _ = om.layer(r[t:t + 1], pos[t:t + 1], k0[:t] if t else None, v0[:t] if t else None,
+                            ls[0], shp, om.bf16_round)
+        _, k, v = om.layer(r1, pos[t:t + 1], None, None, ls[1], shp, om.bf16_round, kv_only=True)
+        k1.append(k[0])
+        v1.append(v[0])
+    assert rel_err(lv[1, 0, ts], np.stack(k1)) <= TOL
+    assert rel_err(lv[1, 1, ts], np.stack(v1)) <= TOL
 
 
 def test_profile_clock_samples_gemm_launches(P):
