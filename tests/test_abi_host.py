@@ -92,6 +92,30 @@ def test_assemble_host_rejections_match_oracle(P, case, code):
         assert e.value.code == code
 
 
+def test_empty_copy_calls_enqueue_nothing(P):
+    """Pack and assemble with no chunks, or only zero-token ones, pass their
+    checks and enqueue nothing: here, with no GPU, they still return OK.
+    An empty header is still checked (a stale epoch rejects the call), as
+    the oracle's assembly checks every header."""
+    h = P.lib()
+    pool = fake_pool(P)
+
+    def pack(descs):
+        arr = (P.ChunkDesc * max(1, len(descs)))(*descs)
+        return P.Status(h.pallas_pack_suffix_blocks(C.byref(pool), FAKE, 4, arr, len(descs), FAKE, 1 << 20,
+                                                    None, None))
+    assert pack([]) == P.Status.OK
+    assert pack([P.ChunkDesc(3, 0, 0), P.ChunkDesc(9, 0, 16)]) == P.Status.OK
+    assert P.Status(assemble_rc(P, [])) == P.Status.OK
+    assert P.Status(assemble_rc(P, [hdr(P, 5, 0), hdr(P, 20, 0, off=64)])) == P.Status.OK
+    assert P.Status(assemble_rc(P, [hdr(P, 5, 0, epoch=2)])) == P.Status.STALE_EPOCH
+    import numpy as np
+    onp = np.zeros((2, 2, 8, 16, 2, 64), np.uint16)
+    with pytest.raises(paged.Rejected) as e:
+        paged.check_chunks(onp, 4 * 16, [paged.ChunkHeader(7, 2, 5, 0, 2, 2, 64, 2)], 7, 3)
+    assert e.value.code == "STALE_EPOCH"
+
+
 def test_pack_host_rejections(P):
     h = P.lib()
     pool = fake_pool(P)

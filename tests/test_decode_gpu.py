@@ -4,12 +4,13 @@ the oracle's cache: one sequence and a batch of three, logits within
 max|gpu - ref| <= 1e-2 max|ref| per row.  At this shape the skinny
 projections split K over workgroups (Q|K|V and gate|up two ways, O and down
 four ways) and reduce the partial sums in the last workgroup of each tile;
-two identical calls give identical logits."""
+two identical calls give identical logits.  Also a token decoding at
+position 0 (an empty cache) in one batch with another sequence."""
 import numpy as np
 import pytest
 import torch
 
-from helpers import TOL, empty_pool, ensure_lib, gpu_model, oracle_weights, rel_err, shape_of
+from helpers import TOL, empty_pool, ensure_lib, gpu_model, kv_logical, oracle_weights, rel_err, shape_of
 from oracle import model as om
 from workloads import configs, gen
 
@@ -60,3 +61,43 @@ def test_decode_large_layer_shape(P):
         assert e <= TOL, f"sequence {i}: logits rel err {e:.3g}"
         if i == 0:
             assert rel_err(one[0].cpu().double().numpy(), ref) <= TOL
+
+
+def test_decode_at_position_zero_in_a_batch(P):
+    """The degenerate context: a token at position 0 over an empty cache
+    attends only to itself.  It decodes in one batch with a sequence at
+    position 20.  Both rows of logits and the K/V each step writes into
+    its slot are checked against the oracle's decode."""
+    cfg = configs.TINY.replace(qk_norm=True)
+    glob, layers = gen.model_weights(cfg, seed=32, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    lens = [0, 20]
+    ids = [gen.token_ids(n + 1, cfg.vocab, seed=32, stream=i).numpy() for i, n in enumerate(lens)]
+    pages = [(n + 1 + 15) // 16 for n in lens]
+    tables = gen.disjoint_block_tables(pages, 8, 2, 32, 1)
+    d_bt = torch.tensor(tables, dtype=torch.int32, device=DEV)
+    pool = empty_pool(cfg, 8, fill_bits=0)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ws = model.workspace(32, 2)
+    model.prefill_prefix(torch.tensor(ids[1][:20], dtype=torch.int32, device=DEV), [0, 20], d_bt[1:2], pool,
+                         ws, err)
+    toks = torch.tensor([x[n] for x, n in zip(ids, lens)], dtype=torch.int32, device=DEV)
+    logits = torch.empty((2, cfg.vocab), dtype=torch.float32, device=DEV)
+    model.decode_step(toks, lens, d_bt, pool, logits, ws, err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    g, ls = oracle_weights(glob, layers)
+    shp = shape_of(cfg)
+    empty = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim))] * cfg.n_layers
+    for i, n in enumerate(lens):
+        if n:
+            K, V, _ = om.prefill(list(ids[i][:n]), g, ls, shp)
+        else:
+            K, V = empty, empty
+        ref, k_new, v_new = om.decode(int(ids[i][n]), n, K, V, g, ls, shp)
+        e = rel_err(logits[i].cpu().double().numpy(), ref)
+        assert e <= TOL, f"sequence {i} at position {n}: logits rel err {e:.3g}"
+        lv = kv_logical(pool, tables[i], n + 1)
+        for l in range(cfg.n_layers):
+            assert rel_err(lv[l, 0, n], k_new[l][0]) <= TOL
+            assert rel_err(lv[l, 1, n], v_new[l][0]) <= TOL
