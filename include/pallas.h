@@ -56,6 +56,7 @@ extern "C" {
 #define PALLAS_ABI_VERSION 3
 #define PALLAS_MAX_SEQS 64 /* sequences per prefill or decode call */
 #define PALLAS_MAX_PREFILL_LEN 32768 /* tokens per sequence in one prefill call */
+#define PALLAS_MAX_DECODE_POS 16383  /* largest position a decode step accepts */
 
 typedef enum {
   PALLAS_OK = 0,
@@ -70,8 +71,10 @@ typedef enum {
 } pallas_status;
 
 /* Device-side error bits written (OR-ed) into the optional d_err word. */
-#define PALLAS_DEVERR_PAGE 1u /* a block-table entry named no page of the pool;
-                                 that position was skipped */
+#define PALLAS_DEVERR_PAGE 1u  /* a block-table entry named no page of the pool;
+                                  that position was skipped */
+#define PALLAS_DEVERR_TOKEN 2u /* a token id outside [0, vocab) (prefill and
+                                  decode); token 0's embedding row was used */
 
 /* Decoder shape (Qwen3/Llama-style pre-norm decoder, Section 6.1 models). */
 typedef struct {
@@ -160,13 +163,25 @@ const char* pallas_last_error(void);
 /* Create a model handle over caller-owned weights (pointers are kept, bytes
  * are not copied).  Fails with INVALID_ARG on a null pointer or inconsistent
  * shape and UNSUPPORTED on a shape without kernels (head_dim other than 64 or
- * 128, page_size other than 16, hidden or ffn not a multiple of 64). */
+ * 128, page_size other than 16, hidden not a multiple of 64, ffn not a
+ * multiple of 16, a GQA group other than 1, 2, 4 or 8 query heads per KV
+ * head). */
 int pallas_model_create(const pallas_model_config* cfg, const pallas_weights* w,
                         pallas_model** out);
 void pallas_model_destroy(pallas_model* m);
 
 /* Bytes of device workspace that prefill and decode need for up to
- * `max_tokens` tokens over up to `max_seqs` sequences in one call. */
+ * `max_tokens` tokens over up to `max_seqs` sequences in one call.
+ *
+ * The workspace (device, 256-byte aligned, owned by the caller) holds the
+ * call's intermediate values.  One part of it is defined, for callers that
+ * validate a model layer by layer: its first rows * hidden float32 values,
+ * row-major [rows][hidden] in the call's row order, are the residual stream.
+ * Once a call's work has completed they hold, after pallas_prefill_prefix
+ * or pallas_prefill_chunk (rows = sum p_i), the residual entering the last
+ * layer (the input of its RMSNorm), and after pallas_decode_step (rows =
+ * num_seqs), the residual leaving the last layer (the input of the final
+ * RMSNorm).  The rest of the workspace is undefined. */
 size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t max_seqs);
 
 /* Prefix prefill (Section 4.3: the target rebuilds the KV cache of the
@@ -182,8 +197,14 @@ size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t 
  * beyond); sum p_i <= the workspace's max_tokens.  One layer's K plane of
  * the pool (num_pages * page * n_kv_heads * head_dim * 2 bytes) must not
  * exceed 4 GiB (UNSUPPORTED): attention addresses it with 32-bit offsets.
+ * For the same reason the projections' bf16 operands must each stay below
+ * 2 GiB (UNSUPPORTED): the call's activation matrices [M][hidden],
+ * [M][n_q_heads * head_dim] and [M][ffn] with M = sum p_i, and the weight
+ * matrices w_qkv, w_o, w_gate_up and w_down.  At hidden 5120, 64 query
+ * heads of 128 and ffn 25600 that caps one call at 41,943 tokens.
  * Table entries outside [0, num_pages) are skipped and raise
- * PALLAS_DEVERR_PAGE in *d_err (nullable, device, caller clears it). */
+ * PALLAS_DEVERR_PAGE, and token ids outside [0, vocab) raise
+ * PALLAS_DEVERR_TOKEN, in *d_err (nullable, device, caller clears it). */
 int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
                           const int32_t* h_cu_seqlens, const int32_t* d_block_tables,
                           int32_t max_pages, const pallas_kv_pool* pool, void* d_workspace,
@@ -203,8 +224,9 @@ int pallas_prefill_prefix(pallas_model* m, int32_t num_seqs, const int32_t* d_to
  * gives the same cache, up to rounding, as one prefill over the whole
  * prefix.  Limits: s_i + p_i <= max_pages * page (OUT_OF_RANGE) and
  * <= PALLAS_MAX_PREFILL_LEN (UNSUPPORTED); sum p_i <= the workspace's
- * max_tokens; the 4 GiB K-plane limit of pallas_prefill_prefix.  Slots [0, s_i) are read, never checked: the caller must
- * have filled them. */
+ * max_tokens; the 4 GiB K-plane and 2 GiB operand limits of
+ * pallas_prefill_prefix.  Slots [0, s_i) are read, never checked: the
+ * caller must have filled them. */
 int pallas_prefill_chunk(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
                          const int32_t* h_cu_seqlens, const int32_t* h_start_pos,
                          const int32_t* d_block_tables, int32_t max_pages,
@@ -253,7 +275,15 @@ int pallas_assemble_kv(const pallas_kv_pool* dst, const int32_t* d_dst_block_tab
  * h_positions[i] = n_i; it attends to cached positions [0, n_i) and to
  * itself, writes its own K/V into slot n_i (the table needs capacity
  * n_i + 1), and the float32 logits of the next token go to
- * d_logits[i][0..V).  num_seqs in [1, PALLAS_MAX_SEQS]. */
+ * d_logits[i][0..V).  num_seqs in [1, PALLAS_MAX_SEQS]; 0 <= n_i <=
+ * PALLAS_MAX_DECODE_POS (UNSUPPORTED beyond: decode attention keeps one
+ * partial record per 64 keys in a workspace section of fixed size), and
+ * n_i + 1 <= max_pages * page (OUT_OF_RANGE).  Up to 8 sequences run the
+ * skinny projection kernel; more run the MFMA GEMM, whose 2 GiB operand
+ * limit (see pallas_prefill_prefix) then also covers lm_head [V][hidden].
+ * Table entries outside [0, num_pages) raise PALLAS_DEVERR_PAGE (the K/V
+ * store of slot n_i is skipped; keys on such pages are masked), token ids
+ * outside [0, vocab) PALLAS_DEVERR_TOKEN, in *d_err (nullable). */
 int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_tokens,
                        const int32_t* h_positions, const int32_t* d_block_tables,
                        int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,

@@ -40,7 +40,7 @@ __global__ __launch_bounds__(kThreads) void embed_rmsnorm_kernel(
   const int t = blockIdx.x;
   int id = ids[t];
   if (id < 0 || id >= vocab) {
-    if (threadIdx.x == 0 && err) atomicOr(err, 2);
+    if (threadIdx.x == 0 && err) atomicOr(err, static_cast<int32_t>(PALLAS_DEVERR_TOKEN));
     id = 0;
   }
   const uint16_t* e = E + static_cast<int64_t>(id) * H;

@@ -15,6 +15,7 @@
 
 static_assert(PALLAS_MAX_SEQS == pallas::kMaxSeqs, "sequence limit");
 static_assert(PALLAS_MAX_PREFILL_LEN == pallas::kMaxPrefillLen, "prefill length limit");
+static_assert(PALLAS_MAX_DECODE_POS == pallas::kDecodeMaxPos - 1, "decode position limit");
 #include "profile.h"
 
 namespace {
@@ -298,6 +299,49 @@ int check_workspace(const pallas_model* m, const void* ws, size_t bytes, int64_t
   return PALLAS_OK;
 }
 
+// The projections address their operands through buffer descriptors with
+// 32-bit byte offsets, so every activation matrix a call feeds them and
+// every weight matrix must stay below 2 GiB (the MFMA GEMM, for more than 8
+// rows), or a 16-row weight tile and 8 activation rows below 4 GiB (the
+// skinny kernel, which decode uses for up to 8 rows; prefill always runs
+// the MFMA GEMM).  Checked here, on the host, so a call that would reach a
+// limit mid-sequence is refused before layer 0 writes anything.
+// `lm_head`: the call also projects the final norm onto the vocabulary
+// (decode).
+int check_gemm_extents(const pallas_model_config& c, int64_t rows, bool skinny, bool lm_head,
+                       const char* what) {
+  const int64_t H = c.hidden, QD = int64_t(c.n_q_heads) * c.head_dim, F = c.ffn;
+  const int64_t QKV = int64_t(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  struct Op {
+    const char* name;
+    int64_t rows, ld;
+  };
+  const Op acts[] = {{"normalised activations", rows, H}, {"attention output", rows, QD},
+                     {"SwiGLU product", rows, F}};
+  const Op wts[] = {{"w_qkv", QKV, H},          {"w_o", H, QD},     {"w_gate_up", 2 * F, H},
+                    {"w_down", H, F},           {"lm_head", lm_head ? int64_t(c.vocab) : 0, H}};
+  if (!skinny) {
+    const int64_t lim = int64_t(1) << 31;
+    for (const Op& o : acts)
+      if (o.rows * o.ld * 2 >= lim)
+        return fail(PALLAS_ERR_UNSUPPORTED, "%s: %lld rows make the %s %lld bytes (at most 2 GiB - 1)", what,
+                    (long long)rows, o.name, (long long)(o.rows * o.ld * 2));
+    for (const Op& o : wts)
+      if (o.rows * o.ld * 2 >= lim)
+        return fail(PALLAS_ERR_UNSUPPORTED, "%s: %s of %lld bytes (at most 2 GiB - 1 for more than 8 rows)", what,
+                    o.name, (long long)(o.rows * o.ld * 2));
+  } else {
+    const int64_t lim = int64_t(1) << 32;
+    for (const Op& o : acts)
+      if (8 * o.ld * 2 >= lim)
+        return fail(PALLAS_ERR_UNSUPPORTED, "%s: %s rows of %lld bytes", what, o.name, (long long)(o.ld * 2));
+    for (const Op& o : wts)
+      if (o.rows > 0 && 16 * o.ld * 2 >= lim)
+        return fail(PALLAS_ERR_UNSUPPORTED, "%s: %s rows of %lld bytes", what, o.name, (long long)(o.ld * 2));
+  }
+  return PALLAS_OK;
+}
+
 #define PALLAS_TRY(cls, expr, where)                  \
   do {                                                \
     pallas::ProfScope ps_(cls, s);                    \
@@ -553,6 +597,7 @@ int prefill_call(pallas_model* m, int32_t num_seqs, const int32_t* d_token_ids,
   }
   const int64_t M = h_cu_seqlens[num_seqs];
   if (M > (int64_t(1) << 24)) return fail(PALLAS_ERR_UNSUPPORTED, "%s: too many tokens", what);
+  if (int rc = check_gemm_extents(m->cfg, M, false, false, what)) return rc;
   if (int rc = check_workspace(m, d_workspace, ws_bytes, M, num_seqs, what)) return rc;
   return run_prefill(m, rm, static_cast<int>(M), d_token_ids, d_block_tables, max_pages, pool,
                      static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));
@@ -604,6 +649,7 @@ int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_token
     rm.base_pos[i] = n;
   }
   rm.cu[num_seqs] = num_seqs;
+  if (int rc = check_gemm_extents(m->cfg, num_seqs, num_seqs <= 8, true, "decode")) return rc;
   if (int rc = check_workspace(m, d_workspace, ws_bytes, num_seqs, num_seqs, "decode")) return rc;
   return run_decode(m, rm, d_tokens, d_block_tables, max_pages, pool, d_logits,
                     static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));

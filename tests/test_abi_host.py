@@ -236,3 +236,79 @@ def test_profile_clock_arguments(P):
     assert h.pallas_profile_clock(7, None, C.byref(wgs)) == P.Status.INVALID_ARG
     assert h.pallas_profile_clock(7, C.byref(ghz), C.byref(wgs)) == P.Status.OK
     assert ghz.value == 0.0 and wgs.value == 0
+
+
+def fake_model(P, c):
+    """A model handle over fake (never dereferenced) weight pointers."""
+    from paper_2608_16477_amd.binding import ModelConfigC, WeightsC, LayerWeightsC
+    h = P.lib()
+    cc = ModelConfigC(c.n_layers, c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn,
+                      c.vocab, c.rms_eps, c.rope_theta, int(c.qk_norm), c.page_size)
+    la = (LayerWeightsC * c.n_layers)()
+    for l in range(c.n_layers):
+        for name, _ in LayerWeightsC._fields_:
+            setattr(la[l], name, FAKE)
+    w = WeightsC(FAKE, FAKE, FAKE, la)
+    model = C.c_void_p()
+    assert h.pallas_model_create(C.byref(cc), C.byref(w), C.byref(model)) == 0
+    return model
+
+
+def test_prefill_rejects_operands_beyond_2_gib(P):
+    """The projections address their bf16 operands with 32-bit offsets, so
+    the [M][ffn] SwiGLU product must stay below 2 GiB: at the 64-layer shape
+    (ffn 25600) a prefill of 41,944 rows (two sequences of 20,972 tokens,
+    within the per-sequence and table limits) is refused on the host with
+    UNSUPPORTED, before anything is enqueued (no device exists here, so any
+    launch would have failed with HIP instead).  41,943 rows pass that check
+    and stop at the undersized workspace.  Both prefill calls apply it."""
+    from workloads import configs
+    from paper_2608_16477_amd.binding import KVPoolC
+    h = P.lib()
+    c = configs.LARGE
+    assert 41943 * c.ffn * 2 < (1 << 31) <= 41944 * c.ffn * 2
+    model = fake_model(P, c)
+    pool = KVPoolC(FAKE, 8192, c.page_size, c.n_layers, c.n_kv_heads, c.head_dim)
+    try:
+        def rc(total, chunk):
+            a = total // 2
+            cu = (C.c_int32 * 3)(0, a, total)
+            if chunk:
+                start = (C.c_int32 * 2)(0, 0)
+                return P.Status(h.pallas_prefill_chunk(model, 2, FAKE, cu, start, FAKE, 2048, C.byref(pool),
+                                                       FAKE, 1 << 40, None, None))
+            return P.Status(h.pallas_prefill_prefix(model, 2, FAKE, cu, FAKE, 2048, C.byref(pool),
+                                                    FAKE, 256, None, None))
+        for chunk in (False, True):
+            assert rc(41944, chunk) == P.Status.UNSUPPORTED
+            assert "SwiGLU product" in P.pallas_last_error()
+        assert rc(41943, False) == P.Status.WORKSPACE
+    finally:
+        h.pallas_model_destroy(model)
+
+
+def test_decode_rejects_positions_and_operands_beyond_limits(P):
+    """Decode positions above PALLAS_MAX_DECODE_POS (16383) are refused with
+    UNSUPPORTED.  More than 8 sequences run the MFMA GEMM, whose operands
+    must stay below 2 GiB: an lm_head of 262144 x 5120 bf16 (2.5 GiB) is
+    refused for 9 sequences and accepted for 8 (the skinny kernel); those
+    calls then stop at the undersized workspace."""
+    from workloads import configs
+    from paper_2608_16477_amd.binding import KVPoolC
+    h = P.lib()
+    c = configs.LARGE.replace(n_layers=2, vocab=262144)
+    model = fake_model(P, c)
+    pool = KVPoolC(FAKE, 8192, c.page_size, c.n_layers, c.n_kv_heads, c.head_dim)
+    try:
+        def rc(positions):
+            pos = (C.c_int32 * len(positions))(*positions)
+            return P.Status(h.pallas_decode_step(model, len(positions), FAKE, pos, FAKE, 2048, C.byref(pool),
+                                                 FAKE, FAKE, 256, None, None))
+        assert rc([16384]) == P.Status.UNSUPPORTED
+        assert "16383" in P.pallas_last_error()
+        assert rc([16383]) == P.Status.WORKSPACE
+        assert rc([10] * 9) == P.Status.UNSUPPORTED
+        assert "lm_head" in P.pallas_last_error()
+        assert rc([10] * 8) == P.Status.WORKSPACE
+    finally:
+        h.pallas_model_destroy(model)
