@@ -100,3 +100,54 @@ def oracle_globals(glob, need_embed_rows=None):
     """Float64 globals; the embedding is gathered to the rows needed."""
     g = {k: to_np64(v) for k, v in glob.items() if k not in ("embed", "lm_head")}
     return g
+
+
+# ------------------------------------------------------------ layer-local parity
+def residual_rows(ws: torch.Tensor, rows: int, hidden: int) -> torch.Tensor:
+    """The residual section of a workspace (pallas.h, pallas_workspace_size):
+    float32 [rows][hidden].  After a prefill it holds the residual entering
+    the model's last layer, after a decode the residual leaving it."""
+    return ws[: rows * hidden * 4].view(torch.float32).view(rows, hidden)
+
+
+def truncated_model(P, cfg, glob, layers, n_layers):
+    """A model handle over the first ``n_layers`` layers of a model (the same
+    device weight tensors)."""
+    return P.Model(cfg.replace(n_layers=n_layers), glob, layers[:n_layers])
+
+
+def check_layer_local(r_in, cu, w, shp, got_k, got_v, r_next=None, tail=None, kv_only=False,
+                      label=""):
+    """Layer-local oracle parity of one decoder layer of a prefill.
+
+    ``r_in [M, H]`` is the residual the GPU fed the layer (float64 of its
+    float32 values), rows of sequence i at ``[cu[i], cu[i+1])`` and
+    positions 0, 1, ...  The oracle runs the layer from that input.  Its K
+    and V of every position must match ``got_k[i], got_v[i] [p_i, Hkv, d]``
+    (the GPU's K/V of the layer) within TOL max|ref| per sequence and
+    tensor.  With ``r_next`` (the GPU's residual leaving the layer), the
+    update the layer adds, r_next - r_in, must match the oracle's within TOL
+    of its max, on every row or on the last ``tail`` rows of each sequence
+    (their attention then reads the oracle's K/V of the earlier rows).
+    Returns the largest relative errors (K, V, update)."""
+    from oracle import model as om
+    worst = [0.0, 0.0, 0.0]
+    for i in range(len(cu) - 1):
+        a, b = cu[i], cu[i + 1]
+        x = r_in[a:b]
+        pos = np.arange(b - a)
+        full = r_next is not None and tail is None
+        r_out, k, v = om.layer(x, pos, None, None, w, shp, om.bf16_round, kv_only=not full)
+        ek, ev = rel_err(got_k[i], k), rel_err(got_v[i], v)
+        worst[0], worst[1] = max(worst[0], ek), max(worst[1], ev)
+        assert ek <= TOL and ev <= TOL, f"{label} sequence {i}: K {ek:.3g}, V {ev:.3g}"
+        if r_next is None or kv_only:
+            continue
+        s = 0 if tail is None else max(0, (b - a) - tail)
+        if not full:
+            r_out, _, _ = om.layer(x[s:], pos[s:], k[:s] if s else None, v[:s] if s else None, w, shp,
+                                   om.bf16_round)
+        eu = rel_err(r_next[a + s:b] - x[s:], r_out - x[s:])
+        worst[2] = max(worst[2], eu)
+        assert eu <= TOL, f"{label} sequence {i}: residual update {eu:.3g}"
+    return worst

@@ -179,3 +179,35 @@ def test_bf16_rounding_drift_is_small():
     for l in range(cfg.n_layers):
         assert np.max(np.abs(K1[l] - K0[l])) <= 1e-2 * np.max(np.abs(K0[l]))
         assert np.max(np.abs(V1[l] - V0[l])) <= 1e-2 * np.max(np.abs(V0[l]))
+
+
+def test_precision_float32_evaluation():
+    """``precision(np.float32)`` evaluates the same forward in float32 and
+    restores float64 on exit.  Pinned against the float64 forward (itself
+    pinned to transformers above): unrounded, the float32 cache and logits
+    agree within float32 accuracy, every result is float32 inside the
+    context and float64 after it; and with bf16 rounding at the stored
+    points (``bf16_round_as``) the float32 cache holds bf16 values."""
+    cfg = small_cfg(True)
+    glob, layers = gen.model_weights(cfg, seed=5, gain_sigma=0.1)
+    ids = gen.token_ids(23, cfg.vocab, seed=5).tolist()
+    g, ls = oracle_weights(glob, layers)
+    shp = shape_of(cfg)
+    K, V, r = om.prefill(ids, g, ls, shp, rnd=on.no_round, full_last=True)
+    lg = om.logits(r, g, shp, rnd=on.no_round)
+    keep = lambda x: x   # noqa: E731  (no rounding, type kept)
+    with om.precision(np.float32):
+        g32 = {k: v.astype(np.float32) for k, v in g.items()}
+        ls32 = [{k: v.astype(np.float32) for k, v in w.items()} for w in ls]
+        K32, V32, r32 = om.prefill(ids, g32, ls32, shp, rnd=keep, full_last=True)
+        lg32 = om.logits(r32, g32, shp, rnd=keep)
+        Kb, _, _ = om.prefill(ids, g32, ls32, shp, rnd=on.bf16_round_as)
+    for a in K32 + V32 + [r32, lg32] + Kb:
+        assert a.dtype == np.float32
+    for a, b in zip(K32 + V32 + [lg32], K + V + [lg]):
+        assert 0 < np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(b))
+    for k in Kb:
+        np.testing.assert_array_equal(k, torch.from_numpy(k).to(torch.bfloat16).float().numpy())
+    K2, _, _ = om.prefill(ids, g, ls, shp, rnd=on.no_round)
+    assert K2[0].dtype == np.float64
+    np.testing.assert_array_equal(K2[0], K[0])

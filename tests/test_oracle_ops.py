@@ -169,3 +169,16 @@ def test_attention_matches_torch_sdpa(Hq, Hkv):
                                          enable_gqa=(Hq != Hkv))[0].permute(1, 0, 2).numpy()
     np.testing.assert_allclose(om.causal_attention(q, np.arange(T), k, v), ref,
                                rtol=1e-10, atol=1e-12)
+
+
+def test_bf16_round_as_keeps_the_type():
+    """bf16 rounding of float32 values stays float32 and equals torch's
+    float32 -> bf16 conversion; of float64 values it equals bf16_round."""
+    x = RNG.standard_normal(50000).astype(np.float32) * np.float32(5.0)
+    got = on.bf16_round_as(x)
+    assert got.dtype == np.float32
+    np.testing.assert_array_equal(got, torch.from_numpy(x).to(torch.bfloat16).float().numpy())
+    y = RNG.standard_normal(1000)
+    got64 = on.bf16_round_as(y)
+    assert got64.dtype == np.float64
+    np.testing.assert_array_equal(got64, on.bf16_round(y))
