@@ -44,8 +44,25 @@ def test_preset_footprints():
     assert configs.LARGE.s_kv == 262144
     assert configs.MID.s_kv == 147456
     assert configs.TINY.s_kv == 1024
-    # copy traffic of the 1000-token large suffix: read + write of the payload
-    assert footprint.copy_traffic_bytes(1000, 64, 8, 128, 2) == 2 * 262144000
+
+
+@pytest.mark.parametrize("n,start", [(1000, 3000), (37, 5)])
+def test_copy_traffic_is_the_packed_payload_read_and_written(n, start):
+    """copy_traffic_bytes against what a pack actually moves: the oracle's
+    brute-force pack of n tokens out of a paged pool yields a chunk whose
+    bytes numpy counts from its shape; each of them is read once from the
+    pool and written once, so the traffic is twice the chunk.  At the large
+    shape and 1000 tokens that is the 524.3 MB of the copy metric."""
+    import numpy as np
+    from oracle import paged
+    L, hkv, d = (64, 8, 128) if n == 1000 else (3, 2, 16)
+    pages = (start + n + 15) // 16
+    pool = np.zeros((L, 2, pages, 16, hkv, d), np.uint16)
+    bt = np.arange(pages)[::-1].copy()
+    chunk = paged.pack(pool, bt, start, n)
+    assert footprint.copy_traffic_bytes(n, L, hkv, d, 2) == 2 * chunk.nbytes
+    if n == 1000:
+        assert 2 * chunk.nbytes == 524288000
 
 
 def test_prefill_flop_count():

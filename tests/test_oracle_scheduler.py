@@ -146,8 +146,17 @@ def test_ewma_geometric():
 
 
 def test_admission():
-    s_kv = 262144.0
-    need = s_kv * (3000 + 25 * 2.0)
-    assert sch.admit(True, need, s_kv, 3000, 25, 2.0)
-    assert not sch.admit(True, need - 1, s_kv, 3000, 25, 2.0)
-    assert not sch.admit(False, 1e15, s_kv, 3000, 25, 2.0)
+    """The state expected at handover is the history the target would have
+    to hold if preparation started at the last moment: Eq. 9's L_hist at a
+    zero window (evaluate), as a KV cache (Eq. 1, footprint.cache_bytes).
+    Admission holds exactly when the free VRAM covers that many bytes, and
+    never for an incompatible model; a handover already due (T_remain <= 0)
+    needs the current context only."""
+    from oracle import footprint
+    rt = sch.Rates(r_p=17500.0, r_d=25.0, B=300e6 / 8, s_kv=262144.0)
+    for K_curr, T_remain in ((3000, 2.0), (4000, 0.0), (1234, -1.0), (10, 7.5)):
+        L0 = sch.evaluate(rt, K_curr, max(T_remain, 0.0), 0.0).L_hist
+        need = footprint.cache_bytes(1, 64, 8, 128, 2) * L0
+        assert sch.admit(True, need, rt.s_kv, K_curr, rt.r_d, T_remain)
+        assert not sch.admit(True, need - 1, rt.s_kv, K_curr, rt.r_d, T_remain)
+        assert not sch.admit(False, 1e15, rt.s_kv, K_curr, rt.r_d, T_remain)
