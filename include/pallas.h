@@ -289,6 +289,31 @@ int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_token
                        int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,
                        void* d_workspace, size_t ws_bytes, int32_t* d_err, void* stream);
 
+/* Decode without a workspace, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  The same step as pallas_decode_step (the same checks,
+ * kernels and results, bit for bit), with its intermediate values in a
+ * scratch array of PALLAS_STATIC_SCRATCH_BYTES that the library keeps in
+ * device memory on each GPU it runs on, from that GPU's first call until
+ * the process ends.  The call allocates nothing; the caller still owns the
+ * tokens, tables, pool and logits.  Every call on one GPU uses that GPU's
+ * one array, so calls whose work overlaps on a GPU (different streams, or
+ * host threads without ordering) race and give undefined results; calls
+ * ordered on one stream do not.  Each call clears what must start at zero.
+ * Limits, beyond those of pallas_decode_step (UNSUPPORTED): at most
+ * PALLAS_STATIC_DECODE_MAX_SEQS sequences, and a scratch need within the
+ * array: roughly num_seqs * n_q_heads * (max n_i / 64 + 1) * (head_dim + 2)
+ * * 4 bytes of attention records plus the step's activations (at 64 query
+ * heads of 128 and ffn 25600: 8 sequences up to position 15,679; fewer
+ * up to 16,383).
+ * HIP on a failed device query. */
+#define PALLAS_STATIC_SCRATCH_BYTES (64u << 20)
+#define PALLAS_STATIC_DECODE_MAX_SEQS 8
+int pallas_decode_step_static(pallas_model* m, int32_t num_seqs, const int32_t* d_tokens,
+                              const int32_t* h_positions, const int32_t* d_block_tables,
+                              int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,
+                              int32_t* d_err, void* stream);
+
 /* Coverage check (Section 4.3, "State consistency"), host only: returns
  * PALLAS_OK iff [0, prefix_len) and the ranges [h_starts[j], h_starts[j] +
  * h_lens[j]) together cover [0, n) exactly once (empty ranges are ignored),

@@ -11,7 +11,7 @@ from .binding import (  # noqa: F401
     pallas_abi_version, pallas_last_error, pallas_check_coverage,
     pallas_model_create, pallas_model_destroy, pallas_workspace_size,
     pallas_prefill_prefix, pallas_prefill_chunk, pallas_pack_suffix_blocks, pallas_assemble_kv,
-    pallas_decode_step, Model, ChunkDesc, ChunkHeader, EXPORTS, KERNEL_CLASSES,
+    pallas_decode_step, pallas_decode_step_static, Model, ChunkDesc, ChunkHeader, EXPORTS, KERNEL_CLASSES,
     pallas_profile_enable, pallas_profile_read, pallas_profile_reset, pallas_profile_clock,
     pallas_window_select, pallas_window_evaluate, pallas_ewma_update, pallas_admit,
     pallas_waste_bound, WindowParams, WindowDecision, Ewma,

@@ -103,6 +103,8 @@ EXPORTS = {
                                      _sz, _i32, _u64, _u64, _vp, _vp]),
     "pallas_decode_step": (C.c_int, [_vp, _i32, _vp, _pi32, _vp, _i32, C.POINTER(KVPoolC), _vp,
                                      _vp, _sz, _vp, _vp]),
+    "pallas_decode_step_static": (C.c_int, [_vp, _i32, _vp, _pi32, _vp, _i32, C.POINTER(KVPoolC), _vp,
+                                            _vp, _vp]),
     "pallas_check_coverage": (C.c_int, [_i32, _pi32, _pi32, _i32, _i32]),
     "pallas_window_evaluate": (C.c_int, [C.POINTER(WindowParams), C.c_double, C.c_double, C.c_double,
                                          C.POINTER(WindowDecision)]),
@@ -261,6 +263,15 @@ def pallas_decode_step(h, tokens, positions: Sequence[int], block_tables, pool, 
                                     _stream(stream)))
 
 
+def pallas_decode_step_static(h, tokens, positions: Sequence[int], block_tables, pool, logits,
+                              err=None, stream=None):
+    """pallas_decode_step with the library's static scratch (no workspace)."""
+    ps = kv_pool_struct(pool)
+    _check(lib().pallas_decode_step_static(h, len(positions), _ptr(tokens), _i32_array(positions),
+                                           _ptr(block_tables), block_tables.shape[-1], C.byref(ps),
+                                           _ptr(logits), _ptr(err), _stream(stream)))
+
+
 def _window_params(r_p, r_d, goodput, s_kv, t_load=0.0, t_0=0.0, alpha=0.8, t_max=5.0, dt=0.01):
     return WindowParams(r_p, r_d, goodput, s_kv, t_load, t_0, alpha, t_max, dt)
 
@@ -366,3 +377,6 @@ class Model:
                     stream=None):
         pallas_decode_step(self.handle, tokens, positions, block_tables, pool, logits, workspace,
                            err, stream)
+
+    def decode_step_static(self, tokens, positions, block_tables, pool, logits, err=None, stream=None):
+        pallas_decode_step_static(self.handle, tokens, positions, block_tables, pool, logits, err, stream)

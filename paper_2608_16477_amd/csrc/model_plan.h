@@ -25,6 +25,7 @@ struct Workspace {
   size_t resid, h, qkv, q, o, act, rope, part, split, split_bytes, attn_split, attn_split_bytes;
   size_t gemv_part, gemv_part_bytes, gemv_ctr;
   int gemv_ctr_count;
+  int part_splits;   // decode attention records per (sequence, query head)
   size_t total;
 };
 
@@ -45,6 +46,7 @@ inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens, 
   w.o = take(size_t(tokens) * c.n_q_heads * c.head_dim * 2);
   w.act = take(size_t(tokens) * c.ffn * 2);
   w.rope = take(size_t(tokens) * (c.head_dim / 2) * 8);  // (cos, sin) per row and pair
+  w.part_splits = kDecodeMaxSplits;
   w.part = take(size_t(seqs) * c.n_q_heads * kDecodeMaxSplits * (c.head_dim + 2) * 4);
   // Split-K partial sums of the projections of up to 256 rows.
   {
@@ -74,6 +76,52 @@ inline Workspace workspace_layout(const pallas_model_config& c, int64_t tokens, 
     w.gemv_ctr_count = static_cast<int>((rows + 15) / 16);
     w.gemv_ctr = take(size_t(w.gemv_ctr_count) * 4);
   }
+  w.total = at;
+  return w;
+}
+
+// The smallest layout a decode step of `seqs` <= 8 sequences needs, with
+// positions up to `max_pos`: the activations, decode-attention records for
+// max_pos / 64 + 1 splits, and the skinny projections' split partial sums
+// and counters at exactly the split counts those projections take (so the
+// arithmetic is that of a step in a full workspace).  No GEMM split-K or
+// prefill-attention section: more than 8 rows are not served from it.
+inline Workspace decode_layout(const pallas_model_config& c, int seqs, int max_pos) {
+  Workspace w{};
+  const int64_t QKV = int64_t(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const int64_t QD = int64_t(c.n_q_heads) * c.head_dim;
+  size_t at = 0;
+  auto take = [&](size_t bytes) { size_t o = at; at = align_up(at + bytes, 256); return o; };
+  w.resid = take(size_t(seqs) * c.hidden * 4);
+  w.h = take(size_t(seqs) * c.hidden * 2);
+  w.qkv = take(size_t(seqs) * QKV * 2);
+  w.q = take(size_t(seqs) * QD * 2);
+  w.o = take(size_t(seqs) * QD * 2);
+  w.act = take(size_t(seqs) * c.ffn * 2);
+  w.rope = take(size_t(seqs) * (c.head_dim / 2) * 8);
+  w.part_splits = max_pos / 64 + 1;
+  w.part = take(size_t(seqs) * c.n_q_heads * w.part_splits * (c.head_dim + 2) * 4);
+  w.split = w.attn_split = 0;
+  w.split_bytes = w.attn_split_bytes = 0;
+  // (epi, N, K) of the five projections; B rows are 2N for gate|up.
+  const int64_t proj[5][3] = {{kEpiBf16, QKV, c.hidden},
+                              {kEpiAddF32, c.hidden, QD},
+                              {kEpiSwiGLU, c.ffn, c.hidden},
+                              {kEpiAddF32, c.hidden, c.ffn},
+                              {kEpiF32, c.vocab, c.hidden}};
+  size_t part = 0;
+  int tiles = 0;
+  for (const auto& pr : proj) {
+    const int S = gemv_ksplit(int(pr[0]), int(pr[1]), int(pr[2]));
+    if (S <= 1) continue;
+    const int64_t nrows = pr[0] == kEpiSwiGLU ? 2 * pr[1] : pr[1];
+    part = std::max(part, size_t(S) * seqs * nrows * 4);
+    tiles = std::max(tiles, int((pr[1] + 15) / 16));
+  }
+  w.gemv_part_bytes = part;
+  w.gemv_part = take(part);
+  w.gemv_ctr_count = tiles;
+  w.gemv_ctr = take(size_t(tiles) * 4);
   w.total = at;
   return w;
 }

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <string>
 #include <cmath>
+#include <mutex>
 #include <vector>
 
 #include "pallas.h"
@@ -470,12 +471,13 @@ int run_prefill(const pallas_model* m, const pallas::RowMap& rm, int M, const in
   return PALLAS_OK;
 }
 
+// One decode step with its intermediate values in `ws`, carved up by `w`
+// (a full workspace's layout, or the compact decode layout).
 int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* tokens, const int32_t* bt,
-               int max_pages, const pallas_kv_pool* pool, float* logits, char* ws, int32_t* err,
-               hipStream_t s) {
+               int max_pages, const pallas_kv_pool* pool, float* logits, char* ws, const pallas::Workspace& w,
+               int32_t* err, hipStream_t s) {
   const pallas_model_config& c = m->cfg;
   const int B = rm.n_seqs;
-  const pallas::Workspace w = pallas::workspace_layout(c, B, B);
   float* part = reinterpret_cast<float*>(ws + w.part);
   float* r = reinterpret_cast<float*>(ws + w.resid);
   uint16_t* h = reinterpret_cast<uint16_t*>(ws + w.h);
@@ -536,7 +538,7 @@ int run_decode(const pallas_model* m, const pallas::RowMap& rm, const int32_t* t
     PALLAS_TRY(PALLAS_K_QKV_EPI, pallas::launch_qkv_rope(qp, rm, B, s), "qkv epilogue");
     ap.k_plane = pl.k;
     ap.v_plane = pl.v;
-    PALLAS_TRY(PALLAS_K_DECODE_ATTN, pallas::launch_attention_decode(ap, rm, part, pallas::kDecodeMaxSplits, s), "decode attention");
+    PALLAS_TRY(PALLAS_K_DECODE_ATTN, pallas::launch_attention_decode(ap, rm, part, w.part_splits, s), "decode attention");
     PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiAddF32, o, QD, u16(L.w_o), QD, r, H, B, H, QD, sc, s), "o proj");
     PALLAS_TRY(PALLAS_K_RMSNORM, pallas::launch_rmsnorm(r, u16(L.mlp_norm), h, B, H, c.rms_eps, s), "rmsnorm");
     PALLAS_TRY(PALLAS_K_DECODE_PROJ, project(pallas::kEpiSwiGLU, h, H, u16(L.w_gate_up), H, act, F, B, F, H, sc, s), "gate_up proj");
@@ -559,6 +561,61 @@ size_t pallas_workspace_size(const pallas_model* m, int32_t max_tokens, int32_t 
 }  // extern "C"
 
 namespace {
+
+// Argument checks shared by both decode entry points; fills the row map.
+int decode_checks(const pallas_model* m, int32_t num_seqs, const int32_t* d_tokens, const int32_t* h_positions,
+                  const int32_t* d_block_tables, int32_t max_pages, const pallas_kv_pool* pool,
+                  const float* d_logits, const char* what, pallas::RowMap& rm) {
+  if (!m) return fail(PALLAS_ERR_INVALID_ARG, "%s: null model", what);
+  if (num_seqs < 1 || num_seqs > PALLAS_MAX_SEQS)
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: num_seqs %d outside [1, %d]", what, num_seqs, PALLAS_MAX_SEQS);
+  if (!d_tokens || !h_positions || !d_block_tables || !d_logits || max_pages <= 0)
+    return fail(PALLAS_ERR_INVALID_ARG, "%s: null tokens, positions, tables or logits", what);
+  if (int rc = check_model_pool(m, pool, what)) return rc;
+  rm.n_seqs = num_seqs;
+  const int64_t cap = int64_t(max_pages) * pool->page_size;
+  for (int i = 0; i < num_seqs; ++i) {
+    rm.cu[i] = i;
+    const int n = h_positions[i];
+    if (n < 0 || int64_t(n) + 1 > cap)
+      return fail(PALLAS_ERR_OUT_OF_RANGE, "%s: position %d of sequence %d outside the table (%lld)", what, n, i,
+                  (long long)cap);
+    if (n >= pallas::kDecodeMaxPos)
+      return fail(PALLAS_ERR_UNSUPPORTED, "%s: position %d beyond %d", what, n, pallas::kDecodeMaxPos - 1);
+    rm.base_pos[i] = n;
+  }
+  rm.cu[num_seqs] = num_seqs;
+  return check_gemm_extents(m->cfg, num_seqs, num_seqs <= 8, true, what);
+}
+
+// Scratch of pallas_decode_step_static: one copy per GPU, in the library's
+// device code object, held until the process ends.  Host code never uses
+// the array's name as an address: its device address on the current GPU is
+// looked up once per device (hipGetSymbolAddress, on the first call that
+// runs there) and kept in `g_scratch`.
+static __device__ __align__(256) unsigned char scratch[PALLAS_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[kMaxDevices];
+
+int static_scratch(char** out) {
+  int dev = -1;
+  if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return hip_fail(e, "decode (static scratch): device");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(PALLAS_ERR_UNSUPPORTED, "decode (static scratch): device %d (at most %d devices)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)); e != hipSuccess)
+      return hip_fail(e, "decode (static scratch): symbol address");
+    if (!p || (reinterpret_cast<uintptr_t>(p) & 255) != 0)
+      return fail(PALLAS_ERR_HIP, "decode (static scratch): bad scratch address");
+    g_scratch[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch[dev];
+  return PALLAS_OK;
+}
 
 // Shared by the whole-prefix and the chunked prefill: sequence i's ids sit
 // at positions start[i] .. start[i] + p_i - 1 (start null: all 0).
@@ -629,30 +686,38 @@ int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_token
                        const int32_t* h_positions, const int32_t* d_block_tables,
                        int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,
                        void* d_workspace, size_t ws_bytes, int32_t* d_err, void* stream) {
-  if (!m) return fail(PALLAS_ERR_INVALID_ARG, "decode: null model");
-  if (num_seqs < 1 || num_seqs > PALLAS_MAX_SEQS)
-    return fail(PALLAS_ERR_INVALID_ARG, "decode: num_seqs %d outside [1, %d]", num_seqs, PALLAS_MAX_SEQS);
-  if (!d_tokens || !h_positions || !d_block_tables || !d_logits || max_pages <= 0)
-    return fail(PALLAS_ERR_INVALID_ARG, "decode: null tokens, positions, tables or logits");
-  if (int rc = check_model_pool(m, pool, "decode")) return rc;
   pallas::RowMap rm;
-  rm.n_seqs = num_seqs;
-  const int64_t cap = int64_t(max_pages) * pool->page_size;
-  for (int i = 0; i < num_seqs; ++i) {
-    rm.cu[i] = i;
-    const int n = h_positions[i];
-    if (n < 0 || int64_t(n) + 1 > cap)
-      return fail(PALLAS_ERR_OUT_OF_RANGE, "decode: position %d of sequence %d outside the table (%lld)", n, i,
-                  (long long)cap);
-    if (n >= pallas::kDecodeMaxPos)
-      return fail(PALLAS_ERR_UNSUPPORTED, "decode: position %d beyond %d", n, pallas::kDecodeMaxPos - 1);
-    rm.base_pos[i] = n;
-  }
-  rm.cu[num_seqs] = num_seqs;
-  if (int rc = check_gemm_extents(m->cfg, num_seqs, num_seqs <= 8, true, "decode")) return rc;
+  if (int rc = decode_checks(m, num_seqs, d_tokens, h_positions, d_block_tables, max_pages, pool, d_logits,
+                             "decode", rm))
+    return rc;
   if (int rc = check_workspace(m, d_workspace, ws_bytes, num_seqs, num_seqs, "decode")) return rc;
-  return run_decode(m, rm, d_tokens, d_block_tables, max_pages, pool, d_logits,
-                    static_cast<char*>(d_workspace), d_err, static_cast<hipStream_t>(stream));
+  return run_decode(m, rm, d_tokens, d_block_tables, max_pages, pool, d_logits, static_cast<char*>(d_workspace),
+                    pallas::workspace_layout(m->cfg, num_seqs, num_seqs), d_err,
+                    static_cast<hipStream_t>(stream));
+}
+
+int pallas_decode_step_static(pallas_model* m, int32_t num_seqs, const int32_t* d_tokens,
+                              const int32_t* h_positions, const int32_t* d_block_tables,
+                              int32_t max_pages, const pallas_kv_pool* pool, float* d_logits,
+                              int32_t* d_err, void* stream) {
+  pallas::RowMap rm;
+  if (int rc = decode_checks(m, num_seqs, d_tokens, h_positions, d_block_tables, max_pages, pool, d_logits,
+                             "decode (static scratch)", rm))
+    return rc;
+  if (num_seqs > PALLAS_STATIC_DECODE_MAX_SEQS)
+    return fail(PALLAS_ERR_UNSUPPORTED, "decode (static scratch): %d sequences (at most %d)", num_seqs,
+                PALLAS_STATIC_DECODE_MAX_SEQS);
+  int max_pos = 0;
+  for (int i = 0; i < num_seqs; ++i) max_pos = std::max(max_pos, h_positions[i]);
+  const pallas::Workspace w = pallas::decode_layout(m->cfg, num_seqs, max_pos);
+  if (w.total > PALLAS_STATIC_SCRATCH_BYTES)
+    return fail(PALLAS_ERR_UNSUPPORTED,
+                "decode (static scratch): %d sequences up to position %d need %zu bytes of scratch (at most %zu)",
+                num_seqs, max_pos, w.total, size_t(PALLAS_STATIC_SCRATCH_BYTES));
+  char* ws = nullptr;
+  if (int rc = static_scratch(&ws)) return rc;
+  return run_decode(m, rm, d_tokens, d_block_tables, max_pages, pool, d_logits, ws, w, d_err,
+                    static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -312,3 +312,32 @@ def test_decode_rejects_positions_and_operands_beyond_limits(P):
         assert rc([10] * 8) == P.Status.WORKSPACE
     finally:
         h.pallas_model_destroy(model)
+
+
+def test_static_decode_host_rejections(P):
+    """pallas_decode_step_static applies pallas_decode_step's checks, then
+    its own limits, all before it touches the device: more than
+    PALLAS_STATIC_DECODE_MAX_SEQS (8) sequences, or a step whose scratch
+    need exceeds PALLAS_STATIC_SCRATCH_BYTES (64 MiB): 8 sequences at
+    position 15,680 of the 64-layer shape need 64.02 MiB.  (A call that
+    passes every check is not made here: with a device present it would
+    launch kernels on the fake pointers.)"""
+    from workloads import configs
+    from paper_2608_16477_amd.binding import KVPoolC
+    h = P.lib()
+    c = configs.LARGE.replace(n_layers=2)
+    model = fake_model(P, c)
+    pool = KVPoolC(FAKE, 8192, c.page_size, c.n_layers, c.n_kv_heads, c.head_dim)
+    try:
+        def rc(positions):
+            pos = (C.c_int32 * len(positions))(*positions)
+            return P.Status(h.pallas_decode_step_static(model, len(positions), FAKE, pos, FAKE, 2048,
+                                                        C.byref(pool), FAKE, None, None))
+        assert rc([16384]) == P.Status.UNSUPPORTED
+        assert rc([5] * 9) == P.Status.UNSUPPORTED
+        assert "at most 8" in P.pallas_last_error()
+        assert rc([15680] * 8) == P.Status.UNSUPPORTED
+        assert "scratch" in P.pallas_last_error()
+        assert rc([-1]) == P.Status.OUT_OF_RANGE
+    finally:
+        h.pallas_model_destroy(model)
