@@ -61,6 +61,32 @@ def gemm_traffic_bytes():
     if sha != t["gemm_source_sha256_16"]:
         return None
     return (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
+
+# Memory-side traffic of pack and assemble (kv_copy_kernel) for the large
+# workload's 1000-token suffix, from the same two counter passes and the
+# same calibration (profiles/kv_copy_traffic.md), KiB per launch after
+# scaling: FETCH_SIZE x 2.0, WRITE_SIZE x 1.0.  Valid only for the copy
+# source it was measured on.
+COPY_TRAFFIC = {
+    "copy_source_sha256_16": "09274b976938982d",
+    "tokens": 1000,
+    "pack": {"fetch_kib": 256139.0, "write_kib": 256000.0},
+    "assemble": {"fetch_kib": 256143.0, "write_kib": 256000.0},
+}
+
+
+def copy_traffic_bytes(kind, suffix_tokens):
+    """HBM bytes of one pack or assemble launch from the stored counters, or
+    None for another copy source or suffix length."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2608_16477_amd", "csrc", "kv_copy.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    t = COPY_TRAFFIC
+    if sha != t["copy_source_sha256_16"] or suffix_tokens != t["tokens"]:
+        return None
+    return (t[kind]["fetch_kib"] + t[kind]["write_kib"]) * 1024.0
+
+
 METRIC = "prefix-prefill tokens/s + % bf16 MFMA peak; KV pack/assemble GB/s + % HBM peak"
 
 
@@ -678,6 +704,21 @@ def cpu_baseline(setup):
     }
 
 
+def copy_roofline(kind, phase_ms, copy_bytes, suffix_tokens, prof):
+    """Pack or assemble against the HBM peak: algorithmic bytes (payload read
+    + written) over the phase's time in the timed steps, the average launch
+    time from the profiled pass, and the counter-measured traffic per launch
+    where it was taken."""
+    ms, n = prof.get(kind, (0.0, 0))
+    traffic = copy_traffic_bytes(kind, suffix_tokens)
+    gbps = copy_bytes / (phase_ms / 1e3) / 1e9
+    return {"bound": "hbm", "bytes": copy_bytes, "ms": phase_ms, "achieved": gbps,
+            "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": gbps / PEAK_HBM_GBPS,
+            "kernel_avg_us": ms / n * 1e3 if n else None,
+            "traffic": traffic,
+            "traffic_ratio": traffic / copy_bytes if traffic else None}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -823,6 +864,18 @@ def main():
             "traffic": gemm_traffic_bytes(),
             "algorithmic_bytes": 2.0 * (prefix_tokens * cfg.hidden + 2 * cfg.ffn * cfg.hidden
                                         + prefix_tokens * cfg.ffn),
+            # The two halves of the metric, each against its own roofline:
+            # the whole prefix prefill (every kernel of the phase) against
+            # the bf16 MFMA peak, and pack / assemble of the suffix payload
+            # (read once + written once) against the HBM peak.
+            "prefill_whole": {
+                "bound": "mfma", "flops": flops, "ms": phase_ms["prefill"],
+                "achieved": flops / (phase_ms["prefill"] / 1e3) / 1e12, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s",
+                "frac": flops / (phase_ms["prefill"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+            },
+            "pack": copy_roofline("pack", phase_ms["pack"], copy_bytes, st.suffix_tokens, prof),
+            "assemble": copy_roofline("assemble", phase_ms["assemble"], copy_bytes, st.suffix_tokens, prof),
         },
         "cpu_baseline": None,
     }
