@@ -30,19 +30,37 @@ namespace pallas {
 
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int kStages = 2;               // LDS ring depth (2 x 64 KiB)
+constexpr int BM = 256, BK = 64;
 constexpr int KK = BK / 16;              // MFMA K-substeps per K-step
 constexpr int kThreads = 512;
 constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
-constexpr int kSlots = BM * kChunks;     // 16-byte slots per operand tile
+constexpr int kSlotsA = BM * kChunks;    // 16-byte slots of the A tile
 // Only waves 0-3 (one per SIMD) issue the operand loads: a wave blocked
 // on a full L1 miss queue cannot issue MFMAs, and this keeps waves 4-7
 // issuing MFMAs on every SIMD.
 constexpr int kLoaderWaves = 4;
-constexpr int kLoads = kSlots / (kLoaderWaves * 64);  // load instructions per loader thread per operand
 constexpr int kXcds = 8;
 constexpr int kGroupM = 6;
+
+// Tile shapes: BN = 256 (8 waves as 2 x 4, each 128 x 64 = 4 x 2 blocks of
+// 32 x 32; a 2-deep LDS ring of 64 KiB stages) or BN = 128 (8 waves as 4 x
+// 2, each 64 x 64 = 2 x 2 blocks; a 3-deep ring of 48 KiB stages, since a
+// half-width step has half the MFMA work to hide its loads behind), for
+// launches whose 256-wide tiles would leave many CUs idle.  Both run the
+// same MFMA over the same K order, so an output element gets the same bits
+// from either.
+template <int BN_>
+struct TileCfg {
+  static constexpr int BN = BN_;
+  static constexpr int kStages = BN_ == 256 ? 2 : 3;
+  static constexpr int WAVES_N = BN_ == 256 ? 4 : 2;
+  static constexpr int WM = BM / (8 / WAVES_N);   // rows per wave
+  static constexpr int WN = BN_ / WAVES_N;        // columns per wave (64)
+  static constexpr int IM = WM / 32, JN = WN / 32;
+  static constexpr int kSlotsB = BN_ * kChunks;
+  static constexpr int kLoadsA = kSlotsA / (kLoaderWaves * 64);   // per loader thread
+  static constexpr int kLoadsB = kSlotsB / (kLoaderWaves * 64);
+};
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -51,20 +69,20 @@ typedef __attribute__((address_space(3))) void lds_void;
 // 4-bank groups.
 __device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 7)); }
 
-// One operand tile's K-step into LDS: kLoads instructions per loader wave;
-// instruction i fills slots [(wave*kLoads+i)*64, +64).  voff[i] is the
-// lane's row offset plus its chunk's column offset, or `limit` for a row
-// past the matrix (the range check then returns zeros).  Without a K tail
-// the step's column offset goes into the scalar offset, so a step costs no
+// One operand tile's K-step into LDS: N instructions per loader wave;
+// instruction i fills slots [(wave*N+i)*64, +64).  voff[i] is the lane's
+// row offset plus its chunk's column offset, or `limit` for a row past the
+// matrix (the range check then returns zeros).  Without a K tail the
+// step's column offset goes into the scalar offset, so a step costs no
 // vector instructions; with one (K not a multiple of BK) each lane checks
 // its column against K.
-template <bool kTail>
+template <int N, bool kTail>
 __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
                                               const uint32_t* voff, const int* kcol, int k0,
                                               int K, u32x4* lds_tile, int wave) {
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    lds_void* dst = (lds_void*)(lds_tile + (wave * kLoads + i) * 64);
+  for (int i = 0; i < N; ++i) {
+    lds_void* dst = (lds_void*)(lds_tile + (wave * N + i) * 64);
     if (kTail) {
       const uint32_t off = (voff[i] < limit && kcol[i] < K - k0) ? voff[i] + static_cast<uint32_t>(k0) * 2u
                                                                  : limit;
@@ -75,14 +93,18 @@ __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint3
   }
 }
 
-template <int EPI>
+template <int EPI, int BN_>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
+  using T = TileCfg<BN_>;
+  constexpr int BN = T::BN, IM = T::IM, JN = T::JN, WM = T::WM, WN = T::WN;
+  constexpr int kLoadsA = T::kLoadsA, kLoadsB = T::kLoadsB;
+  constexpr int kStages = T::kStages, kLoadsStep = kLoadsA + kLoadsB;
   unsigned long long c0 = 0, w0 = 0;
   if (p.clk) {
     c0 = clock64();
     w0 = wall_clock64();
   }
-  __shared__ __attribute__((aligned(16))) u32x4 lds[kStages][2][kSlots];  // [stage][A|B][slot]
+  __shared__ __attribute__((aligned(16))) u32x4 lds[kStages][kSlotsA + T::kSlotsB];  // [stage][A slots, B slots]
 
   const int bid = blockIdx.x;
   const int loc = bid / kXcds;
@@ -107,23 +129,30 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   // Per-thread load plan: byte offset of the row and column chunk each
   // load instruction fills (or the range limit for a row past the matrix),
   // and that chunk's first column.
-  uint32_t a_off[kLoads], b_off[kLoads];
-  int kcol[kLoads];
+  uint32_t a_off[kLoadsA], b_off[kLoadsB];
+  int kcol_a[kLoadsA], kcol_b[kLoadsB];
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    const int s = (wave * kLoads + i) * 64 + lane;
+  for (int i = 0; i < kLoadsA; ++i) {
+    const int s = (wave * kLoadsA + i) * 64 + lane;
     const int row = s / kChunks;
     const int chunk = (s % kChunks) ^ ((row >> 1) & 7);
-    kcol[i] = chunk * 8;
+    kcol_a[i] = chunk * 8;
     const int gm = m0 + row;
     a_off[i] = gm < p.M ? static_cast<uint32_t>(gm * p.lda * 2 + chunk * 16) : p.a_bytes;
+  }
+#pragma unroll
+  for (int i = 0; i < kLoadsB; ++i) {
+    const int s = (wave * kLoadsB + i) * 64 + lane;
+    const int row = s / kChunks;
+    const int chunk = (s % kChunks) ^ ((row >> 1) & 7);
+    kcol_b[i] = chunk * 8;
     int gn;
     bool ok;
     if (EPI == kEpiSwiGLU) {
-      // tile rows [0,128): gate rows o0 + r; [128,256): up rows F + o0 + r - 128
-      const int o = tn * (BN / 2) + (row & 127);
+      // tile rows [0, BN/2): gate rows o0 + r; [BN/2, BN): up rows N + o0 + r - BN/2
+      const int o = tn * (BN / 2) + (row & (BN / 2 - 1));
       ok = o < p.N;
-      gn = (row < 128) ? o : p.N + o;
+      gn = (row < BN / 2) ? o : p.N + o;
     } else {
       gn = tn * BN + row;
       ok = gn < p.N;
@@ -133,20 +162,21 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)p.A, 0, p.a_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)p.B, 0, p.b_bytes, 0x00020000);
 
-  f32x16 acc[4][2];
+  f32x16 acc[IM][JN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < IM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < JN; ++j) acc[i][j] = f32x16{};
 
-  const int wm = wave >> 2, wn = wave & 3;
-  // LDS row of this lane's A fragment i and B fragment j
-  int arow[4], brow[2];
+  const int wm = wave / T::WAVES_N, wn = wave % T::WAVES_N;
+  // LDS row of this lane's A fragment i and B fragment j (B rows follow the
+  // A slots)
+  int arow[IM], brow[JN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) arow[i] = wm * 128 + i * 32 + l32;
+  for (int i = 0; i < IM; ++i) arow[i] = wm * WM + i * 32 + l32;
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
-    brow[j] = (EPI == kEpiSwiGLU ? j * 128 + wn * 32 : wn * 64 + j * 32) + l32;
+  for (int j = 0; j < JN; ++j)
+    brow[j] = (EPI == kEpiSwiGLU ? j * (BN / 2) + wn * 32 : wn * WN + j * 32) + l32;
 
   // K steps [kt0, kt0 + KT) of this unit: the whole K range, or split ks
   // of ksplit near-equal parts.
@@ -154,85 +184,102 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   const int kt0 = ks * KT_all / p.ksplit;
   const int KT = (ks + 1) * KT_all / p.ksplit - kt0;
   const int kb = kt0 * BK;
-  // Prologue: steps 0 and 1 in flight; then step 0 resident.
+  // Prologue: steps 0 .. kStages-1 in flight; then step 0 resident.
   if (wave < kLoaderWaves) {
-    load_tile_lds<true>(ra, p.a_bytes, a_off, kcol, kb, p.K, lds[0][0], wave);
-    load_tile_lds<true>(rb, p.b_bytes, b_off, kcol, kb, p.K, lds[0][1], wave);
-    if (KT > 1) {
-      load_tile_lds<true>(ra, p.a_bytes, a_off, kcol, kb + BK, p.K, lds[1][0], wave);
-      load_tile_lds<true>(rb, p.b_bytes, b_off, kcol, kb + BK, p.K, lds[1][1], wave);
+#pragma unroll
+    for (int st = 0; st < kStages; ++st) {
+      if (st < KT) {
+        load_tile_lds<kLoadsA, true>(ra, p.a_bytes, a_off, kcol_a, kb + st * BK, p.K, lds[st], wave);
+        load_tile_lds<kLoadsB, true>(rb, p.b_bytes, b_off, kcol_b, kb + st * BK, p.K, lds[st] + kSlotsA, wave);
+      }
     }
   }
-  if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoads) : "memory");
+  if (kStages == 3 && KT > 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsStep) : "memory");
+  else if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoadsStep) : "memory");
   else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
 
   // Fragment registers: [substep parity][block]; substep 0 of step kt is
   // read during the last substep of step kt-1.
-  bf16x8 fa[2][4], fb[2][2];
+  bf16x8 fa[2][IM], fb[2][JN];
   auto read_frags = [&](int slot, int kk, bf16x8* a, bf16x8* b) {
-    const u32x4* At = lds[slot][0];
-    const u32x4* Bt = lds[slot][1];
+    const u32x4* At = lds[slot];
+    const u32x4* Bt = lds[slot] + kSlotsA;
     const int c = kk * 2 + g;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = __builtin_bit_cast(bf16x8, At[swz(arow[i], c)]);
+    for (int i = 0; i < IM; ++i) a[i] = __builtin_bit_cast(bf16x8, At[swz(arow[i], c)]);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
+    for (int j = 0; j < JN; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
   };
   auto mfma_block = [&](const bf16x8* a, const bf16x8* b) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < IM; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < JN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   };
   // One LDS read between consecutive MFMAs of a substep ...
   auto sched_reads = [] {
 #pragma unroll
-    for (int q = 0; q < 6; ++q) {
+    for (int q = 0; q < IM + JN; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
     }
   };
-  // ... and, in a loader wave's refill substep, two of its 16 loads as well.
+  // ... and, in a loader wave's refill substep, its loads as well: 16 over
+  // 8 MFMAs (BN 256), 12 over 4 (BN 128).
   auto sched_reads_loads = [] {
+    if constexpr (BN == 256) {
 #pragma unroll
-    for (int q = 0; q < 6; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // 2 global loads
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+      for (int q = 0; q < 6; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // 2 global loads
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 3, 0);  // 3 global loads
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+      }
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
   };
   read_frags(0, 0, fa[0], fb[0]);
 
   // One K-step: MFMAs on substep kk while substep kk+1 is read from slot
-  // kt%2; before the last substep, wait for step kt+1 and barrier.  After
-  // that barrier no wave reads slot kt%2 again, so step kt+2's loads
-  // (kRefill) go there at once, between the last substep's MFMAs, which
-  // also overlap the reads of step kt+1's first substep.  The steady loop
-  // has no branches so the LDS reads interleave with the MFMAs.
+  // kt % kStages; before the last substep, wait for step kt+1 and barrier.
+  // After that barrier no wave reads slot kt % kStages again, so step
+  // kt+kStages's loads (kRefill) go there at once, between the last
+  // substep's MFMAs, which also overlap the reads of step kt+1's first
+  // substep.  The steady loop has no branches so the LDS reads interleave
+  // with the MFMAs.  While refilling, the loads of steps kt+2 ..
+  // kt+kStages-1 may stay in flight at the barrier; in the tail all land.
   auto step = [&](int kt, auto refill_tag, auto loader_tag, auto tail_tag) {
     constexpr bool kRefill = decltype(refill_tag)::value;
     constexpr bool kLoader = decltype(loader_tag)::value;
     constexpr bool kTail = decltype(tail_tag)::value;
-    const int slot = kt & 1;
+    const int slot = kStages == 2 ? (kt & 1) : kt % kStages;
+    const int next = kStages == 2 ? (slot ^ 1) : (slot + 1 == kStages ? 0 : slot + 1);
 #pragma unroll
     for (int kk = 0; kk < KK - 1; ++kk) {
       read_frags(slot, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
       mfma_block(fa[kk & 1], fb[kk & 1]);
       sched_reads();
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (kRefill && kStages == 3) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoadsStep) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     if (kRefill && kLoader) {
-      load_tile_lds<kTail>(ra, p.a_bytes, a_off, kcol, kb + (kt + 2) * BK, p.K, lds[slot][0], wave);
-      load_tile_lds<kTail>(rb, p.b_bytes, b_off, kcol, kb + (kt + 2) * BK, p.K, lds[slot][1], wave);
+      load_tile_lds<kLoadsA, kTail>(ra, p.a_bytes, a_off, kcol_a, kb + (kt + kStages) * BK, p.K, lds[slot], wave);
+      load_tile_lds<kLoadsB, kTail>(rb, p.b_bytes, b_off, kcol_b, kb + (kt + kStages) * BK, p.K,
+                                    lds[slot] + kSlotsA, wave);
     }
     // Step kt+1 is resident; its slot index is valid even past the end
     // (the fragments are then unused).
-    read_frags(slot ^ 1, 0, fa[KK & 1], fb[KK & 1]);
+    read_frags(next, 0, fa[KK & 1], fb[KK & 1]);
     mfma_block(fa[(KK - 1) & 1], fb[(KK - 1) & 1]);
     if (kRefill && kLoader) sched_reads_loads();
     else sched_reads();
@@ -241,7 +288,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   // the same scheduling region as their MFMAs.
   auto main_loop = [&](auto loader_tag, auto tail_tag) {
     int kt = 0;
-    for (; kt + 2 < KT; ++kt) step(kt, std::true_type{}, loader_tag, tail_tag);
+    for (; kt + kStages < KT; ++kt) step(kt, std::true_type{}, loader_tag, tail_tag);
     for (; kt < KT; ++kt) step(kt, std::false_type{}, loader_tag, tail_tag);
   };
   // Only the loader waves issue loads, and only a K that is not a multiple
@@ -251,30 +298,30 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   else main_loop(std::true_type{}, std::true_type{});
 
   // Epilogue.  Accumulator register r of block (i, j) holds
-  // row wm*128 + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.
+  // row wm*WM + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.
   if (p.ksplit > 1) {
     // Split K: the raw float32 sums go to part[ks][row][B row]; the reduce
     // kernel adds the splits in order and applies the epilogue.
     float* P = p.part + static_cast<int64_t>(ks) * p.M * p.part_ld;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < JN; ++j) {
       const int rr = brow[j];  // tile B row (output column) of this lane
       int col;
       bool ok;
       if (EPI == kEpiSwiGLU) {
-        const int o = tn * (BN / 2) + (rr & 127);
+        const int o = tn * (BN / 2) + (rr & (BN / 2 - 1));
         ok = o < p.N;
-        col = (rr < 128) ? o : p.N + o;
+        col = (rr < BN / 2) ? o : p.N + o;
       } else {
         col = tn * BN + rr;
         ok = col < p.N;
       }
       if (!ok) continue;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < IM; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+          const int row = m0 + wm * WM + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
           if (row < p.M) P[static_cast<int64_t>(row) * p.part_ld + col] = acc[i][j][r];
         }
     }
@@ -283,8 +330,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     // rows and columns get an offset past the range, so loads read 0 and
     // stores are dropped without a branch.  Written as C[i] += acc, a load
     // could not pass the previous store (they may alias) and each element
-    // paid a memory round trip; here the 32 residual values of row block
-    // i+1 are loaded before the sums of block i are stored.
+    // paid a memory round trip; here the residual values of row block i+1
+    // are loaded before the sums of block i are stored.
     // (readfirstlane keeps the descriptor in scalar registers; computed in
     // vector registers it would need a loop around every access)
     const int m0s = __builtin_amdgcn_readfirstlane(m0);
@@ -292,22 +339,22 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
         static_cast<float*>(p.C) + static_cast<int64_t>(m0s) * p.ldc, 0, c_bytes, 0x00020000);
     auto off = [&](int i, int r, int j) -> uint32_t {
-      const int row = wm * 128 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-      const int col = tn * BN + wn * 64 + j * 32 + l32;
+      const int row = wm * WM + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+      const int col = tn * BN + wn * WN + j * 32 + l32;
       return col < p.N ? static_cast<uint32_t>(row * p.ldc + col) * 4u : c_bytes;
     };
-    float cv[2][2][16];  // [buffer][j][r]
+    float cv[2][JN][16];  // [buffer][j][r]
     auto load_block = [&](int i, float (*v)[16]) {
 #pragma unroll
       for (int r = 0; r < 16; ++r)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < JN; ++j)
           v[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, off(i, r, j), 0, 0));
     };
     load_block(0, cv[0]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (i + 1 < 4) load_block(i + 1, cv[(i + 1) & 1]);
+    for (int i = 0; i < IM; ++i) {
+      if (i + 1 < IM) load_block(i + 1, cv[(i + 1) & 1]);
       // The sums go back into the accumulators and are stored from there:
       // a store reads its data register late, so storing from cv would make
       // the loads of block i+2 wait for these stores.  (The sum goes through
@@ -317,7 +364,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < JN; ++j) {
           const float sum = cv[i & 1][j][r] + acc[i][j][r];
           acc[i][j][r] = sum;
           __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sum), rc, off(i, r, j), 0, 0);
@@ -325,25 +372,22 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     }
   } else {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < IM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+      const int row = m0 + wm * WM + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
       if (row >= p.M) continue;
       if (EPI == kEpiSwiGLU) {
         uint16_t* C = static_cast<uint16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc;
-#pragma unroll
-        for (int jj = 0; jj < 1; ++jj) {
-          const int col = tn * (BN / 2) + wn * 32 + l32;
-          if (col < p.N) {
-            const float gt = acc[i][0][r], up = acc[i][1][r];
-            C[col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
-          }
+        const int col = tn * (BN / 2) + wn * 32 + l32;
+        if (col < p.N) {
+          const float gt = acc[i][0][r], up = acc[i][1][r];
+          C[col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int col = tn * BN + wn * 64 + j * 32 + l32;
+        for (int j = 0; j < JN; ++j) {
+          const int col = tn * BN + wn * WN + j * 32 + l32;
           if (col >= p.N) continue;
           if (EPI == kEpiF32) {
             float* C = static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc;
@@ -422,9 +466,10 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   p.ldb = ldb;
   p.ldc = ldc;
   p.tiles_m = (M + BM - 1) / BM;
-  p.tiles_n = gemm_tiles_n(epi, N);
-  p.total_tiles = p.tiles_m * p.tiles_n;
   p.ksplit = gemm_ksplit(epi, M, N, K);
+  const int bn = p.ksplit == 1 ? gemm_tile_bn(epi, M, N) : 256;
+  p.tiles_n = gemm_tiles_n(epi, N, bn);
+  p.total_tiles = p.tiles_m * p.tiles_n;
   p.part = part;
   p.part_ld = epi == kEpiSwiGLU ? 2 * N : N;
   if (p.ksplit > 1 && (!part || part_bytes < gemm_split_bytes(epi, M, N, K) || ldc % 4 != 0 ||
@@ -438,13 +483,19 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   p.b_bytes = static_cast<uint32_t>(brows * ldb * 2);
   p.clk = clk;
   const int grid = p.tiles_per_xcd * kXcds;
+#define PALLAS_GEMM_LAUNCH(E)                                                   \
+  case E:                                                                       \
+    if (bn == 128) gemm_bf16_kernel<E, 128><<<grid, kThreads, 0, s>>>(p);       \
+    else gemm_bf16_kernel<E, 256><<<grid, kThreads, 0, s>>>(p);                 \
+    break;
   switch (epi) {
-    case kEpiBf16: gemm_bf16_kernel<kEpiBf16><<<grid, kThreads, 0, s>>>(p); break;
-    case kEpiAddF32: gemm_bf16_kernel<kEpiAddF32><<<grid, kThreads, 0, s>>>(p); break;
-    case kEpiSwiGLU: gemm_bf16_kernel<kEpiSwiGLU><<<grid, kThreads, 0, s>>>(p); break;
-    case kEpiF32: gemm_bf16_kernel<kEpiF32><<<grid, kThreads, 0, s>>>(p); break;
+    PALLAS_GEMM_LAUNCH(kEpiBf16)
+    PALLAS_GEMM_LAUNCH(kEpiAddF32)
+    PALLAS_GEMM_LAUNCH(kEpiSwiGLU)
+    PALLAS_GEMM_LAUNCH(kEpiF32)
     default: return hipErrorInvalidValue;
   }
+#undef PALLAS_GEMM_LAUNCH
   if (p.ksplit > 1) {
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
     const int64_t threads = int64_t(M) * (N / 4);

@@ -63,9 +63,22 @@ struct GemmParams {
   unsigned long long* clk;
 };
 
-// Output-column tiles of one 256-row M tile (gate|up: 128 gate + 128 up
-// columns per tile).
-inline int gemm_tiles_n(int epi, int N) { return epi == kEpiSwiGLU ? (N + 127) / 128 : (N + 255) / 256; }
+// Output-column tiles of one 256-row M tile, for tiles of bn B rows
+// (gate|up: bn/2 gate + bn/2 up rows, so bn/2 output columns per tile).
+inline int gemm_tiles_n(int epi, int N, int bn = 256) {
+  const int cols = epi == kEpiSwiGLU ? bn / 2 : bn;
+  return (N + cols - 1) / cols;
+}
+// B rows per tile: 256, or 128 when 256-row tiles would leave so many of
+// the 256 CUs idle that half-width tiles finish in at most three quarters
+// of the rounds (the mid model's O and down projections at 1536 rows: 96
+// tiles).  The tile width does not change any output bit.
+inline int gemm_tile_bn(int epi, int M, int N) {
+  const int tm = (M + 255) / 256;
+  const int t256 = tm * gemm_tiles_n(epi, N, 256), t128 = tm * gemm_tiles_n(epi, N, 128);
+  const int r256 = (t256 + 255) / 256, r128_x2 = (t128 + 255) / 256;   // rounds of full / half tiles
+  return 4 * r128_x2 <= 6 * r256 ? 128 : 256;                           // 0.5 r128 <= 0.75 r256
+}
 
 // K-range splits per tile.  Only GEMMs of a single 256-row M tile split
 // (their few tiles would leave most of the 256 CUs idle): each split keeps
