@@ -35,12 +35,36 @@ namespace {
 
 constexpr int QB = 32;  // queries per workgroup
 constexpr int KB = 64;  // keys per tile
-constexpr int VPAD = 4; // Vt row padding (elements): 136-byte rows spread banks
 constexpr int kPage = 16;     // tokens per cache page (the only page size the library accepts)
 constexpr int KSTR = KB + 1;  // K tile chunk stride, in 16-byte slots
 constexpr float kLazyLog2 = 8.f;  // lazy-rescale headroom, log2 units
 
 typedef __attribute__((address_space(3))) void lds_void;
+
+// Swizzle of a V tile row's 16-byte chunks: chunk c of key k sits in slot
+// c ^ vswz(k).  The transposed PV reads of one instruction cover 8 keys
+// (two groups of 4 consecutive ones) at 4 chunks each; the XOR puts keys
+// k..k+3 on 4 different quarters of the 256-byte bank window, so 512 bytes
+// read in two passes.
+template <int CH>
+__device__ __forceinline__ int vswz(int key) { return (4 * (key & 3)) & (CH - 1); }
+
+// ds_read_b64_tr_b16 at byte `off` of an LDS tile: in each 16-lane group,
+// lane i receives element i % 4 of the 64-bit words read by lanes i / 4,
+// i / 4 + 4, i / 4 + 8 and i / 4 + 12 of the group, in that order.
+__device__ __forceinline__ u32x2 lds_read_tr16(const u32x4* tile, uint32_t off) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+  typedef __attribute__((address_space(3))) char lds_char;
+  const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)((lds_char*)tile + off));
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// Row-sum step: acc + lo + hi of a packed bf16 pair (a dot product with ones).
+__device__ __forceinline__ float sum_bf2(uint32_t pair, float acc) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pair), ones, acc, false);
+}
 
 struct AttnSched {
   int32_t total;
@@ -68,20 +92,22 @@ template <int D, int G, bool kSplit>
 __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(AttnParams p, RowMap rm, AttnSched sch,
                                                               float* __restrict__ part) {
   constexpr int CH = D / 8;                   // 16-byte chunks per K/V row
-  constexpr int ITEMS = (KB / 2) * CH;        // (key pair, chunk) staging items per tile
-  constexpr int VROW = KB + VPAD;
   constexpr int nthreads = G * 64;
-  constexpr int MAXIT = (ITEMS + nthreads - 1) / nthreads;
-  static_assert(2 * MAXIT <= 16, "wait_vm covers at most 16 outstanding V loads per wave");
+  constexpr int RPI = 64 / CH;                // V rows per staging instruction (64 lanes x 16 B)
+  constexpr int NV = KB / RPI;                // V staging instructions per tile
   static_assert(CH % G == 0, "each wave issues CH / G of a K tile's chunk loads");
+  static_assert(NV % G == 0, "each wave issues NV / G of a V tile's row loads");
   // K tile as [chunk][key] with a chunk stride of KB + 1 slots: the score
-  // MFMA reads 32 consecutive keys of one chunk, and the staging writes of
-  // 16 chunks of one key pair land in distinct banks.
-  // Two K buffers as separate arrays, chosen by a compile-time parity, so
-  // the compiler can tell a tile loading into one from reads of the other.
+  // MFMA reads 32 consecutive keys of one chunk.  V tile as [key][chunk]
+  // (whole head rows) with the 16-byte chunk index XORed by vswz(key), read
+  // transposed (ds_read_b64_tr_b16) into the PV operand.
+  // Two buffers of each as separate arrays, chosen by a compile-time
+  // parity, so the compiler can tell a tile loading into one from reads of
+  // the other.
   __shared__ __attribute__((aligned(16))) u32x4 Ks0[CH * KSTR];
   __shared__ __attribute__((aligned(16))) u32x4 Ks1[CH * KSTR];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VROW];
+  __shared__ __attribute__((aligned(16))) u32x4 Vs0[KB * CH];
+  __shared__ __attribute__((aligned(16))) u32x4 Vs1[KB * CH];
   __shared__ int32_t bts[kMaxPrefillLen / kPage];   // the sequence's block-table entries
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -145,88 +171,51 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
     __syncthreads();
   }
 
-  // Element offsets of key `pos` (and of key pos + 1, same page: pairs start
-  // at even positions and pages hold 16) in a K/V plane, at this KV head.
   // Keys at or past kend are masked for every query of the block; they read
   // key kend - 1 instead (its table entry is staged, and a finite V row
   // times probability zero adds nothing).  A table entry outside the pool
-  // reads page 0 (the K/V store reports such entries).
+  // reads page 0 (the K/V store reports such entries).  K and V planes are
+  // addressed through buffer descriptors with 32-bit offsets (the host
+  // keeps a plane under 4 GiB).
   const int64_t row_stride = static_cast<int64_t>(p.Hkv) * D;
-  const uint16_t* kbase = p.k_plane + kh * D;
-  const uint16_t* vbase = p.v_plane + kh * D;
-  auto pair_off = [&](int pos, int64_t& off0, int64_t& off1) {
+  auto key_off = [&](int pos) -> uint32_t {   // byte offset of key `pos`'s head row in a plane
     const int pc = min(pos, kend - 1);
     int pg = bts[pc >> 4];
     pg = (pg >= 0 && pg < p.num_pages) ? pg : 0;
-    off0 = (static_cast<int64_t>(pg) * kPage + (pc & (kPage - 1))) * row_stride;
-    off1 = off0 + (pos + 1 < kend ? row_stride : 0);
+    return static_cast<uint32_t>((pg * kPage + (pc & (kPage - 1))) * row_stride * 2);
   };
-  // V staging registers: each thread owns MAXIT (key pair, chunk) items.
-  u32x4 svr[MAXIT][2];
-  // V loads this wave issues per tile (threads past the last item issue
-  // none; wave-uniform).
-  int nvload = 0;
-#pragma unroll
-  for (int r = 0; r < MAXIT; ++r)
-    if (wave * 64 + r * nthreads < ITEMS) nvload += 2;
+  const uint32_t head_bytes = static_cast<uint32_t>(p.plane_bytes - static_cast<int64_t>(kh) * D * 2);
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.k_plane + kh * D), 0, head_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.v_plane + kh * D), 0, head_bytes, 0x00020000);
   // K tile straight from memory into LDS: instruction c (16-byte chunk c of
   // the head dimension) has lane l load key k0 + l, so its 64 lanes fill
   // the 64 consecutive slots of chunk c.  Each wave issues CH / G of them.
-  // The K plane is addressed through a buffer descriptor with 32-bit
-  // offsets (the host keeps a plane under 4 GiB).
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)kbase, 0, static_cast<uint32_t>(p.plane_bytes - static_cast<int64_t>(kh) * D * 2), 0x00020000);
   auto dmaK = [&](u32x4* Kd, int k0) {
-    const int pc = min(k0 + lane, kend - 1);
-    int pg = bts[pc >> 4];
-    pg = (pg >= 0 && pg < p.num_pages) ? pg : 0;
-    const uint32_t off = static_cast<uint32_t>((pg * kPage + (pc & (kPage - 1))) * row_stride * 2);
+    const uint32_t off = key_off(k0 + lane);
 #pragma unroll
     for (int i = 0; i < CH / G; ++i) {
       const int ch = wave * (CH / G) + i;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(Kd + ch * KSTR), 16, off + ch * 16, 0, 0, 0);
     }
   };
-  // Wait until at most n of this wave's memory loads are outstanding.
-  auto wait_vm = [](int n) {
-    switch (n) {
-      case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-      case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
-      case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
-      case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
-      case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-      case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
-      case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
-      case 14: asm volatile("s_waitcnt vmcnt(14)" ::: "memory"); break;
-      default: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
-    }
-  };
-  auto gload = [&](u32x4 (&dst)[MAXIT][2], const uint16_t* base, int k0) {
+  // V tile straight into LDS as [key][chunk]: instruction n fills the RPI
+  // rows RPI n .. RPI n + RPI - 1 (lane l: row l / CH, slot l % CH, which
+  // holds logical chunk (l % CH) ^ vswz(row)).  Each wave issues NV / G.
+  const int vrow = lane / CH;   // this lane's row within a staging instruction (RPI n + vrow = vrow mod 4)
+  const uint32_t vcoff = static_cast<uint32_t>(((lane % CH) ^ vswz<CH>(vrow)) * 16);
+  auto dmaV = [&](u32x4* Vd, int k0) {
 #pragma unroll
-    for (int r = 0; r < MAXIT; ++r) {
-      const int it = threadIdx.x + r * nthreads;
-      if (ITEMS % nthreads != 0 && it >= ITEMS) break;
-      const int ch = it % CH, kp = it / CH;  // chunk fastest: lanes read whole head rows
-      int64_t o0, o1;
-      pair_off(k0 + 2 * kp, o0, o1);
-      dst[r][0] = *reinterpret_cast<const u32x4*>(base + o0 + ch * 8);
-      dst[r][1] = *reinterpret_cast<const u32x4*>(base + o1 + ch * 8);
-    }
-  };
-  auto swriteV = [&](int buf) {
-#pragma unroll
-    for (int r = 0; r < MAXIT; ++r) {
-      const int it = threadIdx.x + r * nthreads;
-      if (ITEMS % nthreads != 0 && it >= ITEMS) break;
-      const int ch = it % CH, kp = it / CH;
-      // Vt[dv][key]: keys (2kp, 2kp+1) packed per dv of this chunk
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t a = svr[r][0][e], b = svr[r][1][e];
-        const int key = (2 * kp) ^ (8 * ((ch * 8) >> 5));   // 8-key swizzle by dv / 32
-        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e) * VROW + key]) = __builtin_amdgcn_perm(b, a, 0x05040100u);
-        *reinterpret_cast<uint32_t*>(&Vt[buf][(ch * 8 + 2 * e + 1) * VROW + key]) = __builtin_amdgcn_perm(b, a, 0x07060302u);
-      }
+    for (int i = 0; i < NV / G; ++i) {
+      const int n = wave * (NV / G) + i;
+      // key_off written out: the host pass of this compiler drops the
+      // kernel when the lambda is called inside this loop
+      const int pc = min(k0 + n * RPI + vrow, kend - 1);
+      int pg = bts[pc >> 4];
+      pg = (pg >= 0 && pg < p.num_pages) ? pg : 0;
+      const uint32_t off = static_cast<uint32_t>((pg * kPage + (pc & (kPage - 1))) * row_stride * 2) + vcoff;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(Vd + n * 64), 16, off, 0, 0, 0);
     }
   };
   auto barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
@@ -258,7 +247,11 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
   // Probabilities are exp2((s - m_ref) c).  m_ref is raised only when a
   // score exceeds it by more than kLazyLog2 / c, so probabilities stay below
   // 2^kLazyLog2 and the accumulator is rescaled only on those tiles.
-  float m_ref = -INFINITY, l_run = 0.f;   // l_run: this lane's half of the row sum
+  // Row sums: this lane's keys, in four running partials (one per packed
+  // pair slot of the PV operand), summed over the bf16 probabilities the PV
+  // product uses.
+  float m_ref = -INFINITY;
+  float lsum[4] = {0.f, 0.f, 0.f, 0.f};
   const float c = p.scale_log2;
   const float thr = kLazyLog2 / c;
 
@@ -276,77 +269,79 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
     const float mc = (m_new == -INFINITY) ? 0.f : m_new * c;
     alpha = raise ? __builtin_amdgcn_exp2f(fmaf(m_ref, c, -mc)) : 1.f;
     m_ref = m_new;
-    float rs = 0.f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(st[t][r], c, -mc));
-        st[t][r] = e;
-        rs += e;
-      }
-    l_run = fmaf(l_run, alpha, rs);
+      for (int r = 0; r < 16; ++r) st[t][r] = __builtin_amdgcn_exp2f(fmaf(st[t][r], c, -mc));
     return raise;
   };
-  auto pv = [&](int buf, const f32x16 (&st)[2]) {
-    const uint16_t* Vb = Vt[buf] + l32 * VROW + g * 4;
+  // PV operand A = V^T[dv][16 keys of step cc] from the [key][chunk] tile:
+  // in each 16-lane group, lane j's 64-bit read covers key (4 (lane / 32) +
+  // j / 4) at dimensions dv0 + 4 (j % 4) .. + 3 with dv0 = 32 dt + 16 (j16
+  // % 2), and the transposed read hands lane j of the group that key
+  // quartet's dimension dv0 + j: 4 consecutive keys of one output row.  Two
+  // reads (keys + 0 and + 8) give the 8 keys the score registers hold for
+  // that lane, in the same order.  Byte offsets within a tile, for cc = 0:
+  const int j16 = lane & 15, grp = lane >> 4;
+  uint32_t voff[D / 32];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt) {
+    const int key = 4 * g + j16 / 4;
+    const int lc = dt * 4 + 2 * (grp & 1) + (j16 & 3) / 2;   // logical 16-byte chunk
+    voff[dt] = static_cast<uint32_t>(key * D * 2 + ((lc ^ vswz<CH>(key)) * 16) + (j16 & 1) * 8);
+  }
+  auto pv = [&](const u32x4* Vsrc, const f32x16 (&st)[2]) {
 #pragma unroll
     for (int cc = 0; cc < KB / 16; ++cc) {
       const int t = cc >> 1, base = (cc & 1) * 8;
       u32x4 pk;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pk[e] = pack_bf2(st[t][base + 2 * e], st[t][base + 2 * e + 1]);
+      for (int e = 0; e < 4; ++e) {
+        pk[e] = pack_bf2(st[t][base + 2 * e], st[t][base + 2 * e + 1]);
+        lsum[e] = sum_bf2(pk[e], lsum[e]);
+      }
       const bf16x8 pb = __builtin_bit_cast(bf16x8, pk);
-      // The swizzle XORs the key with 8 dt (dt = dv / 32): 16-key block cc
-      // sits at block cc ^ (dt / 2), and with odd dt its upper 8 keys come
-      // first.  The two 8-byte halves are read in address order, and odd
-      // rows take the probabilities with their halves swapped (a sum is
-      // order-free), so no register moves precede the MFMA.
-      const bf16x8 pb_swap = __builtin_bit_cast(bf16x8, u32x4{pk[2], pk[3], pk[0], pk[1]});
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        // keys cc*16 + g*4 + {0..3} and + 8, at their swizzled slots
-        const uint16_t* vrow = Vb + dt * 32 * VROW + (cc ^ (dt >> 1)) * 16;
-        const u32x2 a0 = *reinterpret_cast<const u32x2*>(vrow);
-        const u32x2 a1 = *reinterpret_cast<const u32x2*>(vrow + 8);
-        const u32x4 av = {a0.x, a0.y, a1.x, a1.y};
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), (dt & 1) ? pb_swap : pb,
-                                                           oacc[dt], 0, 0, 0);
+        const u32x2 l2 = lds_read_tr16(Vsrc, voff[dt] + cc * 16 * D * 2);
+        const u32x2 h2 = lds_read_tr16(Vsrc, voff[dt] + (cc * 16 + 8) * D * 2);
+        const u32x4 av = {l2.x, l2.y, h2.x, h2.y};
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pb, oacc[dt], 0, 0, 0);
       }
     }
   };
   auto rescale = [&](float alpha) {
 #pragma unroll
     for (int t = 0; t < D / 32; ++t) oacc[t] *= alpha;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) lsum[e] *= alpha;
   };
 
   // Pipeline: while tile j's softmax runs, tile j+1's scores are computed
   // from its K tile (already in LDS).  K tiles go straight to LDS two tiles
-  // ahead; V tiles are loaded into registers one tile ahead and written
-  // transposed.
+  // ahead, V tiles one tile ahead.
   dmaK(Ks0, kt0);
+  dmaV(Vs0, kt0);
   if (ntiles > 1) dmaK(Ks1, kt0 + KB);
-  gload(svr, vbase, kt0);
-  swriteV(0);
-  if (ntiles > 1) gload(svr, vbase, kt0 + KB);
-  wait_vm(ntiles > 1 ? nvload : 0);   // K_0 and K_1 have landed
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   barrier();
   // One pipeline step: scores of tile j+1 into `nxt` while tile j (scores in
   // `cur`, wholly below the diagonal) goes through softmax and PV.  B = j % 2
-  // is a template constant: K_j sat in buffer B, K_{j+1} sits in 1 - B.
+  // is a template constant: K_j and V_j sit in buffer B, K_{j+1} in 1 - B.
   auto step = [&](auto parity, int j, f32x16 (&cur)[2], f32x16 (&nxt)[2]) {
     constexpr int B = decltype(parity)::value;
     u32x4* Kfree = B == 0 ? Ks0 : Ks1;
     const u32x4* Knext = B == 0 ? Ks1 : Ks0;
+    const u32x4* Vcur = B == 0 ? Vs0 : Vs1;
+    u32x4* Vnext = B == 0 ? Vs1 : Vs0;
     barrier();   // K_{j+1} and V_j resident; the buffers of K_j and V_{j-1} free
     if (j + 2 < ntiles) dmaK(Kfree, kt0 + (j + 2) * KB);
+    dmaV(Vnext, kt0 + (j + 1) * KB);   // j + 1 < ntiles here
     scores(Knext, nxt);
     float alpha;
     if (softmax(cur, alpha)) rescale(alpha);
-    pv(B, cur);
-    swriteV(1 - B);
-    if (j + 2 < ntiles) gload(svr, vbase, kt0 + (j + 2) * KB);
-    wait_vm(j + 2 < ntiles ? nvload : 0);   // K_{j+2} lands before the next barrier
+    pv(Vcur, cur);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // K_{j+2}, V_{j+1} land before the next barrier
   };
   f32x16 sa[2], sb[2];
   scores(Ks0, sa);
@@ -375,10 +370,10 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
       }
     float alpha;
     if (softmax(st, alpha)) rescale(alpha);
-    pv((ntiles - 1) & 1, st);
+    pv(((ntiles - 1) & 1) ? Vs1 : Vs0, st);
   }
 
-  const float l_tot = xhalf_sum(l_run);
+  const float l_tot = xhalf_sum((lsum[0] + lsum[1]) + (lsum[2] + lsum[3]));
   if (!qvalid) return;
   if (kSplit) {
 #pragma unroll
