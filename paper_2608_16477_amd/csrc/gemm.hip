@@ -93,8 +93,22 @@ __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint3
   }
 }
 
-template <int EPI, int BN_>
-__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
+
+template <int BN_>
+using LdsRing = u32x4[TileCfg<BN_>::kStages][kSlotsA + TileCfg<BN_>::kSlotsB];   // [stage][A slots, B slots]
+
+// How a workgroup finds its work unit.  Workgroups are dealt round-robin
+// over the 8 XCDs; XCD x owns the contiguous run of units
+// [x tiles_per_xcd, +tiles_per_xcd).  kUnitsPlain: unit = (tile, K split)
+// of one width.  kUnitsTailFull / kUnitsTailHalf (gemm_bf16_tail_kernel):
+// the last tail_half full tiles of a run are split into two half-width
+// units each, which follow the run's full tiles.
+enum { kUnitsPlain = 0, kUnitsTailFull = 1, kUnitsTailHalf = 2 };
+
+// One workgroup: its unit, then the output tile (M tile tm, column tile tn
+// of BN_ B rows) over its K split, with its LDS ring `lds`.
+template <int EPI, int BN_, int kUnits>
+__device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>& lds) {
   using T = TileCfg<BN_>;
   constexpr int BN = T::BN, IM = T::IM, JN = T::JN, WM = T::WM, WN = T::WN;
   constexpr int kLoadsA = T::kLoadsA, kLoadsB = T::kLoadsB;
@@ -104,14 +118,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     c0 = clock64();
     w0 = wall_clock64();
   }
-  __shared__ __attribute__((aligned(16))) u32x4 lds[kStages][kSlotsA + T::kSlotsB];  // [stage][A slots, B slots]
-
   const int bid = blockIdx.x;
   const int loc = bid / kXcds;
-  if (loc >= p.tiles_per_xcd) return;
-  const int u = (bid % kXcds) * p.tiles_per_xcd + loc;   // work unit: (tile, K split)
-  if (u >= p.total_tiles * p.ksplit) return;
-  const int t = u / p.ksplit, ks = u % p.ksplit;
+  int t, ks = 0, half = 0;
+  if (kUnits == kUnitsPlain) {
+    if (loc >= p.tiles_per_xcd) return;
+    const int u = (bid % kXcds) * p.tiles_per_xcd + loc;   // work unit: (tile, K split)
+    if (u >= p.total_tiles * p.ksplit) return;
+    t = u / p.ksplit;
+    ks = u % p.ksplit;
+  } else {
+    const int full = p.tiles_per_xcd - p.tail_half;
+    if (kUnits == kUnitsTailFull) {
+      t = (bid % kXcds) * p.tiles_per_xcd + loc;
+    } else {
+      t = (bid % kXcds) * p.tiles_per_xcd + full + (loc - full) / 2;
+      half = (loc - full) % 2;
+    }
+    if (t >= p.total_tiles) return;
+  }
   // Grouped order: runs of group_m M-tiles, M fastest, so the ~32
   // workgroups an XCD runs at once cover about group_m x (32 / group_m)
   // tiles and share both operand panels in its L2.
@@ -119,7 +144,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
   const int first_m = (t / per_group) * p.group_m;
   const int gsz = min(p.tiles_m - first_m, p.group_m);
   const int tm = first_m + (t % per_group) % gsz;
-  const int tn = (t % per_group) / gsz;
+  const int tn = (kUnits == kUnitsTailHalf ? 2 : 1) * ((t % per_group) / gsz) + half;
   const int m0 = tm * BM;
 
   const int lane = threadIdx.x & 63;
@@ -330,8 +355,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     // rows and columns get an offset past the range, so loads read 0 and
     // stores are dropped without a branch.  Written as C[i] += acc, a load
     // could not pass the previous store (they may alias) and each element
-    // paid a memory round trip; here the residual values of row block i+1
-    // are loaded before the sums of block i are stored.
+    // paid a memory round trip; here the residual values of the next half
+    // block are loaded before the sums of this one are stored.
     // (readfirstlane keeps the descriptor in scalar registers; computed in
     // vector registers it would need a loop around every access)
     const int m0s = __builtin_amdgcn_readfirstlane(m0);
@@ -343,31 +368,34 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
       const int col = tn * BN + wn * WN + j * 32 + l32;
       return col < p.N ? static_cast<uint32_t>(row * p.ldc + col) * 4u : c_bytes;
     };
-    float cv[2][JN][16];  // [buffer][j][r]
-    auto load_block = [&](int i, float (*v)[16]) {
+    // Half blocks q = (block i = q / 2, rows 8 (q % 2) .. + 8) are double
+    // buffered (32 registers; whole blocks would take 64).
+    float cv[2][JN][8];  // [buffer][j][r]
+    auto load_half = [&](int q, float (*v)[8]) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
+      for (int r = 0; r < 8; ++r)
 #pragma unroll
         for (int j = 0; j < JN; ++j)
-          v[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, off(i, r, j), 0, 0));
+          v[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, off(q >> 1, (q & 1) * 8 + r, j), 0, 0));
     };
-    load_block(0, cv[0]);
+    load_half(0, cv[0]);
 #pragma unroll
-    for (int i = 0; i < IM; ++i) {
-      if (i + 1 < IM) load_block(i + 1, cv[(i + 1) & 1]);
+    for (int q = 0; q < 2 * IM; ++q) {
+      if (q + 1 < 2 * IM) load_half(q + 1, cv[(q + 1) & 1]);
       // The sums go back into the accumulators and are stored from there:
       // a store reads its data register late, so storing from cv would make
-      // the loads of block i+2 wait for these stores.  (The sum goes through
-      // a temporary: writing acc[i][j][r] and reading it back in the same
-      // unrolled loop was miscompiled by the ROCm 7.2 clang; a probe stored
-      // element 0's sum for every r.)
+      // the loads of the next half block wait for these stores.  (The sum
+      // goes through a temporary: writing acc[i][j][r] and reading it back
+      // in the same unrolled loop was miscompiled by the ROCm 7.2 clang; a
+      // probe stored element 0's sum for every r.)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
+      for (int r = 0; r < 8; ++r)
 #pragma unroll
         for (int j = 0; j < JN; ++j) {
-          const float sum = cv[i & 1][j][r] + acc[i][j][r];
-          acc[i][j][r] = sum;
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sum), rc, off(i, r, j), 0, 0);
+          const int i = q >> 1, rr = (q & 1) * 8 + r;
+          const float sum = cv[q & 1][j][r] + acc[i][j][rr];
+          acc[i][j][rr] = sum;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sum), rc, off(i, rr, j), 0, 0);
         }
     }
   } else {
@@ -407,6 +435,26 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
     atomicAdd(&p.clk[1], w1 - w0);
     atomicAdd(&p.clk[2], 1ull);
   }
+}
+
+// Tiles of one width.
+template <int EPI, int BN_>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) LdsRing<BN_> lds;
+  gemm_workgroup<EPI, BN_, kUnitsPlain>(p, lds);
+}
+
+// Full-width tiles with a split tail: the last p.tail_half full tiles of
+// each XCD's run (its last, partly filled round) run as two half-width
+// tiles each, so that round ends sooner.  Same bits as full-width tiles.
+template <int EPI>
+__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_tail_kernel(GemmParams p) {
+  static_assert(sizeof(LdsRing<128>) >= sizeof(LdsRing<256>), "the half-width ring is the larger");
+  __shared__ __attribute__((aligned(16))) LdsRing<128> lds;
+  const int loc = static_cast<int>(blockIdx.x) / kXcds;
+  if (loc >= p.tiles_per_xcd + p.tail_half) return;
+  if (loc >= p.tiles_per_xcd - p.tail_half) gemm_workgroup<EPI, 128, kUnitsTailHalf>(p, lds);
+  else gemm_workgroup<EPI, 256, kUnitsTailFull>(p, reinterpret_cast<LdsRing<256>&>(lds));
 }
 
 // Split-K reduction: C = epilogue(sum over ks of part[ks]), the splits
@@ -477,15 +525,23 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
                        (reinterpret_cast<uintptr_t>(C) & 15) != 0))
     return hipErrorInvalidValue;
   p.tiles_per_xcd = (p.total_tiles * p.ksplit + kXcds - 1) / kXcds;
+  // A last round that keeps at most half of an XCD's 32 CUs busy runs as
+  // half-width tiles (full-width launches without a K split only).
+  p.tail_half = 0;
+  if (bn == 256 && p.ksplit == 1) {
+    const int rounds = (p.tiles_per_xcd + 31) / 32, last = p.tiles_per_xcd - 32 * (rounds - 1);
+    if (rounds > 1 && last <= 16) p.tail_half = last;
+  }
   p.group_m = std::min(p.tiles_m, kGroupM);
   p.a_bytes = static_cast<uint32_t>(int64_t(M) * lda * 2);
   const int64_t brows = epi == kEpiSwiGLU ? 2 * int64_t(N) : N;
   p.b_bytes = static_cast<uint32_t>(brows * ldb * 2);
   p.clk = clk;
-  const int grid = p.tiles_per_xcd * kXcds;
+  const int grid = (p.tiles_per_xcd + p.tail_half) * kXcds;
 #define PALLAS_GEMM_LAUNCH(E)                                                   \
   case E:                                                                       \
     if (bn == 128) gemm_bf16_kernel<E, 128><<<grid, kThreads, 0, s>>>(p);       \
+    else if (p.tail_half) gemm_bf16_tail_kernel<E><<<grid, kThreads, 0, s>>>(p);\
     else gemm_bf16_kernel<E, 256><<<grid, kThreads, 0, s>>>(p);                 \
     break;
   switch (epi) {

@@ -54,6 +54,7 @@ struct GemmParams {
   int M, N, K;
   int lda, ldb, ldc;
   int tiles_m, tiles_n, total_tiles, tiles_per_xcd, group_m;
+  int tail_half;        // full tiles per XCD run split into two half-width tiles (tail kernel)
   int ksplit;           // K-range splits per tile (1: none)
   float* part;          // split partial sums [ksplit][M][part_ld] (ksplit > 1)
   int part_ld;          // B rows: N, or 2N for the gate|up product
