@@ -40,16 +40,16 @@ NOMINAL_SCLK_GHZ = 2.4      # clock the MFMA peak is quoted at
 # Memory-side traffic of one gate|up GEMM launch at the large workload, from
 # two rocprofv3 --pmc passes over `bench.py --steps 1 --warmup 0
 # --no-cpu-baseline --no-stress --no-chunked --no-staging` (FETCH_SIZE, then
-# WRITE_SIZE, KiB per dispatch, averaged
-# over the gate|up launches at M = 3000), each scaled by what the same counter
+# WRITE_SIZE, KiB per dispatch, averaged over the gate|up launches at
+# M = 3000; profiles/gemm_attention_counters.md), each scaled by what the same counter
 # reads for a 1 GiB device copy (`bench.py --copy-calibration`: FETCH_SIZE
 # x 2.0, WRITE_SIZE x 1.0).  Valid
 # only for the GEMM source it was measured on: a different csrc/gemm.hip
 # reports null.
 GEMM_TRAFFIC = {
-    "gemm_source_sha256_16": "783867caba7038fc",
-    "fetch_kib": 1.309e6, "fetch_scale": 2.0,
-    "write_kib": 1.502e5, "write_scale": 1.0,
+    "gemm_source_sha256_16": "3a09db3e248aada4",
+    "fetch_kib": 1.34463e6, "fetch_scale": 2.0,
+    "write_kib": 1.50234e5, "write_scale": 1.0,
 }
 
 
