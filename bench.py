@@ -253,6 +253,37 @@ def copies_stress(P, seed):
         torch.cuda.synchronize()
         return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3
 
+    def same(a, b, what):
+        if not torch.equal(a.view(torch.uint8), b.view(torch.uint8)):
+            raise RuntimeError(f"graph replay of {what} differs from the eager call")
+
+    def graph_us(fn, check, calls=20, reps=10):
+        """Device time per call: `calls` calls captured in one graph (the
+        copies enqueue no memset and allocate nothing), the graph replayed
+        back to back; median over `reps` event-timed replays, divided by
+        `calls`.  The host-side marshalling that the single-call figure
+        includes is outside.  `check()` compares the replayed result with
+        the eager one, before and after the timed replays."""
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(calls):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        check()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for a, b in evs:
+            a.record()
+            g.replay()
+            b.record()
+        torch.cuda.synchronize()
+        check()
+        del g
+        return float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3 / calls
+
     rows = []
     for s in configs.STRESS_SUFFIXES:
         start = n_src - s
@@ -262,27 +293,47 @@ def copies_stress(P, seed):
             descs.append(P.ChunkDesc(t, c, k * configs.STRESS_CHUNK * row))
             hdrs.append(P.ChunkHeader(7, 1, t, c, k * configs.STRESS_CHUNK * row, L, hkv, d, 2))
         nbytes = 2 * s * row
-        t_pack = median_us(lambda: P.pallas_pack_suffix_blocks(src, src_bt, descs, arena, err))
-        t_asm = median_us(lambda: P.pallas_assemble_kv(dst, dst_bt, hdrs, arena, 7, 1, err))
+        do_pack = lambda: P.pallas_pack_suffix_blocks(src, src_bt, descs, arena, err)
+        do_asm = lambda: P.pallas_assemble_kv(dst, dst_bt, hdrs, arena, 7, 1, err)
+        t_pack = median_us(do_pack)
+        t_asm = median_us(do_asm)
         # practical ceiling: a plain contiguous device copy of the same payload
         # (torch's copy kernel), timed the same way
         ca = arena[: s * row]
         cb = torch.empty_like(ca)
         t_copy = median_us(lambda: cb.copy_(ca))
-        del cb
+        # the same three, replayed from a graph
+        packed = ca.clone()
+        dst_pages = dst_bt[start // cfg.page_size: n_src // cfg.page_size].long()
+        assembled = dst[:, :, dst_pages].clone()
+
+        g_pack = graph_us(do_pack, lambda: same(ca, packed, "pack"))
+        g_asm = graph_us(do_asm, lambda: same(dst[:, :, dst_pages], assembled, "assemble"))
+        g_copy = graph_us(lambda: cb.copy_(ca), lambda: same(cb, ca, "device copy"))
+        del cb, packed, assembled
+        frac = lambda us: nbytes / us / 1e3 / PEAK_HBM_GBPS
         rows.append({"suffix_tokens": s, "chunks_per_launch": len(descs), "bytes": nbytes,
                      "pack_us": t_pack, "pack_GBps": nbytes / t_pack / 1e3,
-                     "pack_hbm_frac": nbytes / t_pack / 1e3 / PEAK_HBM_GBPS,
+                     "pack_hbm_frac": frac(t_pack),
                      "assemble_us": t_asm, "assemble_GBps": nbytes / t_asm / 1e3,
-                     "assemble_hbm_frac": nbytes / t_asm / 1e3 / PEAK_HBM_GBPS,
-                     "device_copy_us": t_copy, "device_copy_hbm_frac": nbytes / t_copy / 1e3 / PEAK_HBM_GBPS})
+                     "assemble_hbm_frac": frac(t_asm),
+                     "device_copy_us": t_copy, "device_copy_hbm_frac": frac(t_copy),
+                     "graph": {"pack_us": g_pack, "pack_hbm_frac": frac(g_pack),
+                               "assemble_us": g_asm, "assemble_hbm_frac": frac(g_asm),
+                               "device_copy_us": g_copy, "device_copy_hbm_frac": frac(g_copy)}})
     # one launch per 32-token chunk
     c = configs.STRESS_CHUNK
     one_d = [P.ChunkDesc(n_src - c, c, 0)]
     one_h = [P.ChunkHeader(7, 1, n_src - c, c, 0, L, hkv, d, 2)]
+    one_pack = lambda: P.pallas_pack_suffix_blocks(src, src_bt, one_d, arena, err)
+    one_asm = lambda: P.pallas_assemble_kv(dst, dst_bt, one_h, arena, 7, 1, err)
     lat = {"chunk_tokens": c, "bytes": 2 * c * row,
-           "pack_us": median_us(lambda: P.pallas_pack_suffix_blocks(src, src_bt, one_d, arena, err)),
-           "assemble_us": median_us(lambda: P.pallas_assemble_kv(dst, dst_bt, one_h, arena, 7, 1, err))}
+           "pack_us": median_us(one_pack), "assemble_us": median_us(one_asm)}
+    packed = arena[: c * row].clone()
+    pages = dst_bt[(n_src - c) // cfg.page_size: n_src // cfg.page_size].long()
+    assembled = dst[:, :, pages].clone()
+    lat["graph_pack_us"] = graph_us(one_pack, lambda: same(arena[: c * row], packed, "pack"))
+    lat["graph_assemble_us"] = graph_us(one_asm, lambda: same(dst[:, :, pages], assembled, "assemble"))
     torch.cuda.synchronize()
     assert int(err.item()) == 0, "device-side error flag raised in the stress copies"
     return {"layout": (f"{L} layers, {hkv} KV heads, head_dim {d}: {n_src}-token source in "

@@ -69,8 +69,46 @@ __device__ __forceinline__ float sum_bf2(uint32_t pair, float acc) {
 struct AttnSched {
   int32_t total;
   int32_t split_tiles;           // key tiles per split (split launches)
-  int32_t prefix[kMaxSeqs + 1];  // query blocks before sequence s
+  int32_t last_block;            // largest absolute query block of the call
 };
+
+// Dispatch order of the (query block, head group) workgroups.  Workgroups
+// start in linear grid order, each on the first CU of its XCD that frees
+// up, so the order decides the balance: a query block's causal key range
+// grows with its absolute block index, and ranking every block of every
+// sequence by that index, largest first, with the head groups of a block
+// consecutive, makes the dispatch longest-job-first over the whole call.
+// Rank r is the block B with count(>= B) > r >= count(>= B + 1), where
+// count(>= b) sums over sequences the blocks at index b or later; ties go
+// in sequence order.
+__host__ __device__ __forceinline__ void block_of_rank(const RowMap& rm, const AttnSched& sch, int r, int& s_out,
+                                              int& b_out) {
+  if (rm.n_seqs == 1) {
+    s_out = 0;
+    b_out = sch.last_block - r;
+    return;
+  }
+  auto count_ge = [&](int b) {
+    int c = 0;
+    for (int s = 0; s < rm.n_seqs; ++s) {
+      const int f = rm.base_pos[s] / QB, l = (rm.base_pos[s] + rm.cu[s + 1] - rm.cu[s] - 1) / QB;
+      c += max(0, l - max(f, b) + 1);
+    }
+    return c;
+  };
+  int lo = 0, hi = sch.last_block + 1;   // count_ge(lo) > r >= count_ge(hi)
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (count_ge(mid) > r) lo = mid; else hi = mid;
+  }
+  int k = r - count_ge(lo + 1), s = 0;
+  for (;; ++s) {
+    const int f = rm.base_pos[s] / QB, l = (rm.base_pos[s] + rm.cu[s + 1] - rm.cu[s] - 1) / QB;
+    if (f <= lo && lo <= l && k-- == 0) break;
+  }
+  s_out = s;
+  b_out = lo;
+}
 
 // Full max / sum over the two 32-lane halves of a wave (the two key halves
 // of one query in the S^T layout).
@@ -112,14 +150,16 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int g = lane >> 5, l32 = lane & 31;
-  // Workgroup y covers query heads [y G, y G + G), all of one KV head (G
-  // divides the group size Hq / Hkv).
-  const int h = static_cast<int>(blockIdx.y) * G + wave;
+  // Workgroup x is head group x mod (Hq / G), query block of rank
+  // x / (Hq / G) (block_of_rank).  Head group y covers query heads
+  // [y G, y G + G), all of one KV head (G divides the group size Hq / Hkv).
+  const int ngroups = p.Hq / G;
+  const int h = (static_cast<int>(blockIdx.x) % ngroups) * G + wave;
   const int kh = __builtin_amdgcn_readfirstlane(h / (p.Hq / p.Hkv));
-
-  const int gidx = sch.total - 1 - static_cast<int>(blockIdx.x);  // longest blocks first
-  int s = 0;
-  while (s + 1 < rm.n_seqs && sch.prefix[s + 1] <= gidx) ++s;
+  int s, qblock;
+  block_of_rank(rm, sch, static_cast<int>(blockIdx.x) / ngroups, s, qblock);
+  s = __builtin_amdgcn_readfirstlane(s);
+  qblock = __builtin_amdgcn_readfirstlane(qblock);
   // Query blocks sit at absolute positions [32 b, 32 b + 32): the rows of
   // sequence s are positions [base, base + len), so with base > 0 (a chunk
   // over earlier chunks) the first block may be partly before the chunk.
@@ -128,7 +168,7 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
   // undivided prefill would.
   const int base = rm.base_pos[s];
   const int len = rm.cu[s + 1] - rm.cu[s];
-  const int q0 = ((base / QB) + (gidx - sch.prefix[s])) * QB;
+  const int q0 = qblock * QB;
   const int row0 = rm.cu[s] - base;   // row of absolute position a: row0 + a
   const int32_t* bt = p.bt + static_cast<int64_t>(s) * p.max_pages;
 
@@ -640,16 +680,16 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnParams p, Ro
 hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, float* part, size_t part_bytes,
                                    hipStream_t s) {
   AttnSched sch;
-  sch.prefix[0] = 0;
+  sch.total = 0;
   int maxlen = 0;
   for (int i = 0; i < rm.n_seqs; ++i) {
     const int len = rm.cu[i + 1] - rm.cu[i], base = rm.base_pos[i];
     if (len < 1 || base < 0) return hipErrorInvalidValue;
     maxlen = std::max(maxlen, base + len);
-    sch.prefix[i + 1] = sch.prefix[i] + (base + len + QB - 1) / QB - base / QB;
+    sch.total += (base + len + QB - 1) / QB - base / QB;
   }
-  sch.total = sch.prefix[rm.n_seqs];
   if (sch.total == 0) return hipSuccess;
+  sch.last_block = (maxlen - 1) / QB;
   // Query heads per workgroup: the whole GQA group, except that a group of
   // 8 at head_dim 128 is split over two 4-wave workgroups (two of which fit
   // on a CU) when the call has fewer than 512 (query block, KV head) pairs,
@@ -664,7 +704,7 @@ hipError_t launch_attention_prefill(const AttnParams& p, const RowMap& rm, float
   sch.split_tiles = (((maxlen + KB - 1) / KB) + S - 1) / S;
   if (S > 1 && (!part || part_bytes < attn_prefill_split_bytes(rows, p.Hq, p.d)))
     return hipErrorInvalidValue;
-  dim3 grid(sch.total, p.Hq / G, S);
+  dim3 grid(sch.total * (p.Hq / G), 1, S);
 #define PALLAS_ATTN_CASE(DD, GG)                                                                 \
   if (p.d == DD && G == GG) {                                                                    \
     if (S == 1) {                                                                                \
