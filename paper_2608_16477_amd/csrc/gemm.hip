@@ -4,7 +4,11 @@
 //
 // Tiling: a 256 x 256 output tile per workgroup of 8 waves (two per SIMD,
 // so one wave's barrier and LDS waits overlap the other's MFMAs), each wave
-// 128 x 64 as 4 x 2 blocks of v_mfma_f32_32x32x16_bf16.  K advances 64 at
+// 128 x 64 as 8 x 4 blocks of v_mfma_f32_16x16x32_bf16.  The 16 x 16 x 32
+// shape moves half the accumulator bits per FLOP of the 32 x 32 x 16 one,
+// which matters because the chip runs these GEMMs at its power limit: a
+// register-only loop of each over all CUs, with random operands, held
+// 2.0 GHz and 1.99 PFLOP/s against 1.76 GHz and 1.80 PFLOP/s.  K advances 64 at
 // a time through a double-buffered LDS stage (2 x (32 KiB A + 32 KiB B))
 // filled by buffer loads that write LDS directly (no register staging);
 // one barrier per step.  Step kt+2's loads are issued right after the
@@ -31,7 +35,7 @@ namespace pallas {
 namespace {
 
 constexpr int BM = 256, BK = 64;
-constexpr int KK = BK / 16;              // MFMA K-substeps per K-step
+constexpr int KK = BK / 32;              // MFMA K-substeps per K-step
 constexpr int kThreads = 512;
 constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
 constexpr int kSlotsA = BM * kChunks;    // 16-byte slots of the A tile
@@ -42,9 +46,9 @@ constexpr int kLoaderWaves = 4;
 constexpr int kXcds = 8;
 constexpr int kGroupM = 6;
 
-// Tile shapes: BN = 256 (8 waves as 2 x 4, each 128 x 64 = 4 x 2 blocks of
-// 32 x 32; a 2-deep LDS ring of 64 KiB stages) or BN = 128 (8 waves as 4 x
-// 2, each 64 x 64 = 2 x 2 blocks; a 3-deep ring of 48 KiB stages, since a
+// Tile shapes: BN = 256 (8 waves as 2 x 4, each 128 x 64 = 8 x 4 blocks of
+// 16 x 16; a 2-deep LDS ring of 64 KiB stages) or BN = 128 (8 waves as 4 x
+// 2, each 64 x 64 = 4 x 4 blocks; a 3-deep ring of 48 KiB stages, since a
 // half-width step has half the MFMA work to hide its loads behind), for
 // launches whose 256-wide tiles would leave many CUs idle.  Both run the
 // same MFMA over the same K order, so an output element gets the same bits
@@ -56,7 +60,7 @@ struct TileCfg {
   static constexpr int WAVES_N = BN_ == 256 ? 4 : 2;
   static constexpr int WM = BM / (8 / WAVES_N);   // rows per wave
   static constexpr int WN = BN_ / WAVES_N;        // columns per wave (64)
-  static constexpr int IM = WM / 32, JN = WN / 32;
+  static constexpr int IM = WM / 16, JN = WN / 16;
   static constexpr int kSlotsB = BN_ * kChunks;
   static constexpr int kLoadsA = kSlotsA / (kLoaderWaves * 64);   // per loader thread
   static constexpr int kLoadsB = kSlotsB / (kLoaderWaves * 64);
@@ -69,30 +73,37 @@ typedef __attribute__((address_space(3))) void lds_void;
 // 4-bank groups.
 __device__ __forceinline__ int swz(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 7)); }
 
-// One operand tile's K-step into LDS: N instructions per loader wave;
-// instruction i fills slots [(wave*N+i)*64, +64).  voff[i] is the lane's
-// row offset plus its chunk's column offset, or `limit` for a row past the
-// matrix (the range check then returns zeros).  Without a K tail the
-// step's column offset goes into the scalar offset, so a step costs no
-// vector instructions; with one (K not a multiple of BK) each lane checks
-// its column against K.
+// Operand loads into LDS.  A loader wave issues N load instructions per
+// operand tile and K-step; instruction i fills slots [(wave*N+i)*64, +64),
+// tile rows 8 (wave N + i) + lane / 8.  The lane's chunk swizzle depends on
+// i only through its parity, so the lane keeps two offsets, voff[0..1]
+// (its row's byte offset plus its chunk's column offset for instructions
+// 0 and 1), and instruction i adds the 8 (i - i mod 2) rows past those,
+// `step` bytes each, in a vector register computed at the load (16 offsets
+// kept live would cost registers that the accumulators need).  The range check thus sees the
+// whole row offset: a row past the matrix reads zeros.  Without a K tail
+// the step's column offset goes into the scalar offset; with one (K not a
+// multiple of BK) each lane checks its column against K.
 template <int N, bool kTail>
-__device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
-                                              const uint32_t* voff, const int* kcol, int k0,
-                                              int K, u32x4* lds_tile, int wave) {
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-    lds_void* dst = (lds_void*)(lds_tile + (wave * N + i) * 64);
-    if (kTail) {
-      const uint32_t off = (voff[i] < limit && kcol[i] < K - k0) ? voff[i] + static_cast<uint32_t>(k0) * 2u
-                                                                 : limit;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, off, 0, 0, 0);
-    } else {
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, voff[i], k0 * 2, 0, 0);
-    }
+__device__ __forceinline__ void load_row_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
+                                             const uint32_t* voff, const int* kcol, uint32_t step,
+                                             int k0, int K, u32x4* lds_tile, int wave, int i) {
+  lds_void* dst = (lds_void*)(lds_tile + (wave * N + i) * 64);
+  const uint32_t vo = voff[i & 1] + static_cast<uint32_t>(i & ~1) * step;
+  if (kTail) {
+    const uint32_t off = kcol[i & 1] < K - k0 ? vo + static_cast<uint32_t>(k0) * 2u : limit;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, off, 0, 0, 0);
+  } else {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, dst, 16, vo, k0 * 2, 0, 0);
   }
 }
-
+template <int N, bool kTail>
+__device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint32_t limit,
+                                              const uint32_t* voff, const int* kcol, uint32_t step,
+                                              int k0, int K, u32x4* lds_tile, int wave) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) load_row_lds<N, kTail>(rsrc, limit, voff, kcol, step, k0, K, lds_tile, wave, i);
+}
 
 template <int BN_>
 using LdsRing = u32x4[TileCfg<BN_>::kStages][kSlotsA + TileCfg<BN_>::kSlotsB];   // [stage][A slots, B slots]
@@ -149,59 +160,64 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 5, l32 = lane & 31;
+  // MFMA lane roles: lane l supplies row l mod 16 of a 16-row operand
+  // block and its K elements [8 q4, 8 q4 + 8) of the 32-element substep;
+  // accumulator register r holds row 4 q4 + r, column l mod 16.
+  const int q4 = lane >> 4, l16 = lane & 15;
 
-  // Per-thread load plan: byte offset of the row and column chunk each
-  // load instruction fills (or the range limit for a row past the matrix),
-  // and that chunk's first column.
-  uint32_t a_off[kLoadsA], b_off[kLoadsB];
-  int kcol_a[kLoadsA], kcol_b[kLoadsB];
+  // Per-thread load plan (load_tile_lds): the byte offsets of the lane's
+  // row and column chunk for an even and an odd load instruction, and the
+  // chunk's first column.  Rows past M (A) and past the weight's rows (B)
+  // lie past the buffer's range and read zeros.  In the SwiGLU launch's
+  // last column tile, gate rows past N read up rows instead: they feed
+  // only output columns past N, which are never stored.  (A wave's B rows
+  // lie all in the gate half or all in the up half.)
+  uint32_t a_off[2], b_off[2];
+  int kcol_a[2], kcol_b[2];
 #pragma unroll
-  for (int i = 0; i < kLoadsA; ++i) {
+  for (int i = 0; i < 2; ++i) {
     const int s = (wave * kLoadsA + i) * 64 + lane;
     const int row = s / kChunks;
     const int chunk = (s % kChunks) ^ ((row >> 1) & 7);
     kcol_a[i] = chunk * 8;
-    const int gm = m0 + row;
-    a_off[i] = gm < p.M ? static_cast<uint32_t>(gm * p.lda * 2 + chunk * 16) : p.a_bytes;
+    a_off[i] = static_cast<uint32_t>((m0 + row) * p.lda * 2 + chunk * 16);
   }
 #pragma unroll
-  for (int i = 0; i < kLoadsB; ++i) {
+  for (int i = 0; i < 2; ++i) {
     const int s = (wave * kLoadsB + i) * 64 + lane;
     const int row = s / kChunks;
     const int chunk = (s % kChunks) ^ ((row >> 1) & 7);
     kcol_b[i] = chunk * 8;
     int gn;
-    bool ok;
     if (EPI == kEpiSwiGLU) {
       // tile rows [0, BN/2): gate rows o0 + r; [BN/2, BN): up rows N + o0 + r - BN/2
       const int o = tn * (BN / 2) + (row & (BN / 2 - 1));
-      ok = o < p.N;
       gn = (row < BN / 2) ? o : p.N + o;
     } else {
       gn = tn * BN + row;
-      ok = gn < p.N;
     }
-    b_off[i] = ok ? static_cast<uint32_t>(gn * p.ldb * 2 + chunk * 16) : p.b_bytes;
+    b_off[i] = static_cast<uint32_t>(gn * p.ldb * 2 + chunk * 16);
   }
+  static_assert(kLoadsA % 2 == 0 && kLoadsB % 2 == 0, "loads come in even/odd pairs");
+  static_assert(BN / 2 % (8 * kLoadsB) == 0, "a wave's B rows stay in one half");
+  const uint32_t a_step = 8u * p.lda * 2u, b_step = 8u * p.ldb * 2u;
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)p.A, 0, p.a_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)p.B, 0, p.b_bytes, 0x00020000);
 
-  f32x16 acc[IM][JN];
+  f32x4 acc[IM][JN];
 #pragma unroll
   for (int i = 0; i < IM; ++i)
 #pragma unroll
-    for (int j = 0; j < JN; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < JN; ++j) acc[i][j] = f32x4{};
 
   const int wm = wave / T::WAVES_N, wn = wave % T::WAVES_N;
-  // LDS row of this lane's A fragment i and B fragment j (B rows follow the
-  // A slots)
-  int arow[IM], brow[JN];
-#pragma unroll
-  for (int i = 0; i < IM; ++i) arow[i] = wm * WM + i * 32 + l32;
-#pragma unroll
-  for (int j = 0; j < JN; ++j)
-    brow[j] = (EPI == kEpiSwiGLU ? j * (BN / 2) + wn * 32 : wn * WN + j * 32) + l32;
+  // LDS row of this lane's A fragment i, arow0 + 16 i, and B fragment j,
+  // brow0 + bblk(j) (B rows follow the A slots).
+  const int arow0 = wm * WM + l16;
+  const int brow0 = (EPI == kEpiSwiGLU ? wn * (WN / 2) : wn * WN) + l16;
+  auto bblk = [](int j) {
+    return EPI == kEpiSwiGLU ? (j / (JN / 2)) * (BN / 2) + (j % (JN / 2)) * 16 : j * 16;
+  };
 
   // K steps [kt0, kt0 + KT) of this unit: the whole K range, or split ks
   // of ksplit near-equal parts.
@@ -214,8 +230,9 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
 #pragma unroll
     for (int st = 0; st < kStages; ++st) {
       if (st < KT) {
-        load_tile_lds<kLoadsA, true>(ra, p.a_bytes, a_off, kcol_a, kb + st * BK, p.K, lds[st], wave);
-        load_tile_lds<kLoadsB, true>(rb, p.b_bytes, b_off, kcol_b, kb + st * BK, p.K, lds[st] + kSlotsA, wave);
+        load_tile_lds<kLoadsA, true>(ra, p.a_bytes, a_off, kcol_a, a_step, kb + st * BK, p.K, lds[st], wave);
+        load_tile_lds<kLoadsB, true>(rb, p.b_bytes, b_off, kcol_b, b_step, kb + st * BK, p.K, lds[st] + kSlotsA,
+                                     wave);
       }
     }
   }
@@ -224,90 +241,89 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
   else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
 
-  // Fragment registers: [substep parity][block]; substep 0 of step kt is
-  // read during the last substep of step kt-1.
-  bf16x8 fa[2][IM], fb[2][JN];
-  auto read_frags = [&](int slot, int kk, bf16x8* a, bf16x8* b) {
-    const u32x4* At = lds[slot];
-    const u32x4* Bt = lds[slot] + kSlotsA;
-    const int c = kk * 2 + g;
+  // Fragment registers.  B is double-buffered by substep parity, A is
+  // single-buffered.  Substep 0 of step kt is read during the last
+  // substep of step kt-1.  Every fragment row is congruent to l16 mod 16,
+  // so the swizzle term (row / 2) mod 8 is the same for all of this lane's
+  // blocks.
+  // A fragment i of substep kk sits at slot's A base + arow0 rows +
+  // ((4 kk + q4) XOR xsw) chunks + 16 i rows: one lane address per
+  // (slot, substep) and an immediate offset per block.
+  bf16x8 fa[IM], fb[2][JN];
+  const int xsw = (l16 >> 1) & 7;
+  auto abase = [&](int slot, int kk) { return lds[slot] + arow0 * kChunks + ((kk * 4 + q4) ^ xsw); };
+  auto bbase = [&](int slot, int kk) { return lds[slot] + kSlotsA + brow0 * kChunks + ((kk * 4 + q4) ^ xsw); };
+  auto frag = [](const u32x4* base, int rows) { return __builtin_bit_cast(bf16x8, base[rows * kChunks]); };
+  {
+    const u32x4* Ab = abase(0, 0);   // substep 0 of step 0 (slot 0)
+    const u32x4* Bb = bbase(0, 0);
 #pragma unroll
-    for (int i = 0; i < IM; ++i) a[i] = __builtin_bit_cast(bf16x8, At[swz(arow[i], c)]);
+    for (int i = 0; i < IM; ++i) fa[i] = frag(Ab, i * 16);
 #pragma unroll
-    for (int j = 0; j < JN; ++j) b[j] = __builtin_bit_cast(bf16x8, Bt[swz(brow[j], c)]);
-  };
-  auto mfma_block = [&](const bf16x8* a, const bf16x8* b) {
+    for (int j = 0; j < JN; ++j) fb[0][j] = frag(Bb, bblk(j));
+  }
+  // One substep: the MFMAs on fa and bc, in groups of one A block (JN
+  // MFMAs), each followed by that block's re-read for the next substep
+  // (substep kk of `slot`; its last use is just done), one of the next
+  // substep's B blocks into bn while any remain, and, in a loader wave's
+  // refill substep, kPer of its operand loads for K-step `kload` into
+  // `lslot`.  A scheduling fence closes each group, so a block's re-read
+  // cannot move above its MFMAs (which would need a second A buffer) and
+  // the loads spread over the substep.
+  constexpr int kPer = kLoadsStep / IM;
+  static_assert(kPer * IM == kLoadsStep && JN <= IM, "loads and B reads spread over the A groups");
+  auto substep = [&](const bf16x8* bc, int slot, int kk, bf16x8* bn, auto loads_tag, auto tail_tag, int kload,
+                     int lslot) {
+    constexpr bool kLoads = decltype(loads_tag)::value;
+    constexpr bool kTail = decltype(tail_tag)::value;
+    const u32x4* Ab = abase(slot, kk);
+    const u32x4* Bb = bbase(slot, kk);
 #pragma unroll
-    for (int i = 0; i < IM; ++i)
+    for (int i = 0; i < IM; ++i) {
 #pragma unroll
       for (int j = 0; j < JN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-  };
-  // One LDS read between consecutive MFMAs of a substep ...
-  auto sched_reads = [] {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], bc[j], acc[i][j], 0, 0, 0);
+      if (i < JN) bn[i] = frag(Bb, bblk(i));
+      fa[i] = frag(Ab, i * 16);
+      if constexpr (kLoads) {
 #pragma unroll
-    for (int q = 0; q < IM + JN; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+        for (int q = i * kPer; q < (i + 1) * kPer; ++q) {
+          if (q < kLoadsA)
+            load_row_lds<kLoadsA, kTail>(ra, p.a_bytes, a_off, kcol_a, a_step, kload, p.K, lds[lslot], wave, q);
+          else
+            load_row_lds<kLoadsB, kTail>(rb, p.b_bytes, b_off, kcol_b, b_step, kload, p.K, lds[lslot] + kSlotsA,
+                                         wave, q - kLoadsA);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // ... and, in a loader wave's refill substep, its loads as well: 16 over
-  // 8 MFMAs (BN 256), 12 over 4 (BN 128).
-  auto sched_reads_loads = [] {
-    if constexpr (BN == 256) {
-#pragma unroll
-      for (int q = 0; q < 6; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-        __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // 2 global loads
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-        __builtin_amdgcn_sched_group_barrier(0x020, 3, 0);  // 3 global loads
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-      }
-    }
-  };
-  read_frags(0, 0, fa[0], fb[0]);
 
-  // One K-step: MFMAs on substep kk while substep kk+1 is read from slot
-  // kt % kStages; before the last substep, wait for step kt+1 and barrier.
+  // One K-step: the substeps of slot kt % kStages, each reading the next
+  // one's fragments; before the last, wait for step kt+1 and barrier.
   // After that barrier no wave reads slot kt % kStages again, so step
-  // kt+kStages's loads (kRefill) go there at once, between the last
-  // substep's MFMAs, which also overlap the reads of step kt+1's first
-  // substep.  The steady loop has no branches so the LDS reads interleave
-  // with the MFMAs.  While refilling, the loads of steps kt+2 ..
-  // kt+kStages-1 may stay in flight at the barrier; in the tail all land.
+  // kt+kStages's loads (kRefill) go there at once, spread over the last
+  // substep, which also reads step kt+1's first substep.  While
+  // refilling, the loads of steps kt+2 .. kt+kStages-1 may stay in flight
+  // at the barrier; in the tail all land.
   auto step = [&](int kt, auto refill_tag, auto loader_tag, auto tail_tag) {
     constexpr bool kRefill = decltype(refill_tag)::value;
     constexpr bool kLoader = decltype(loader_tag)::value;
-    constexpr bool kTail = decltype(tail_tag)::value;
     const int slot = kStages == 2 ? (kt & 1) : kt % kStages;
     const int next = kStages == 2 ? (slot ^ 1) : (slot + 1 == kStages ? 0 : slot + 1);
+    // Opaque to the optimiser each step, so the per-load offset sums stay
+    // at the loads instead of being hoisted out of the loop.
+    if constexpr (kRefill && kLoader) asm volatile("" : "+v"(a_off[0]), "+v"(a_off[1]), "+v"(b_off[0]), "+v"(b_off[1]));
 #pragma unroll
-    for (int kk = 0; kk < KK - 1; ++kk) {
-      read_frags(slot, kk + 1, fa[(kk + 1) & 1], fb[(kk + 1) & 1]);
-      mfma_block(fa[kk & 1], fb[kk & 1]);
-      sched_reads();
-    }
+    for (int kk = 0; kk < KK - 1; ++kk)
+      substep(fb[kk & 1], slot, kk + 1, fb[(kk + 1) & 1], std::false_type{}, tail_tag, 0, 0);
     if (kRefill && kStages == 3) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoadsStep) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
-    if (kRefill && kLoader) {
-      load_tile_lds<kLoadsA, kTail>(ra, p.a_bytes, a_off, kcol_a, kb + (kt + kStages) * BK, p.K, lds[slot], wave);
-      load_tile_lds<kLoadsB, kTail>(rb, p.b_bytes, b_off, kcol_b, kb + (kt + kStages) * BK, p.K,
-                                    lds[slot] + kSlotsA, wave);
-    }
     // Step kt+1 is resident; its slot index is valid even past the end
     // (the fragments are then unused).
-    read_frags(next, 0, fa[KK & 1], fb[KK & 1]);
-    mfma_block(fa[(KK - 1) & 1], fb[(KK - 1) & 1]);
-    if (kRefill && kLoader) sched_reads_loads();
-    else sched_reads();
+    substep(fb[(KK - 1) & 1], next, 0, fb[KK & 1], std::integral_constant<bool, kRefill && kLoader>{}, tail_tag,
+            kb + (kt + kStages) * BK, slot);
   };
   // The K-loop is specialised per role so the loader waves' loads sit in
   // the same scheduling region as their MFMAs.
@@ -323,14 +339,20 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
   else main_loop(std::true_type{}, std::true_type{});
 
   // Epilogue.  Accumulator register r of block (i, j) holds
-  // row wm*WM + i*32 + (r/4)*8 + g*4 + r%4 and column (block col) + l32.
+  // row wm*WM + i*16 + 4*q4 + r and column (block col) + l16.  The lane
+  // roles are derived again from an opaque copy of the thread index, so
+  // nothing computed before the K-loop stays live through it for the
+  // epilogue (the loop needs every register it has).
+  int tid_e = static_cast<int>(threadIdx.x);
+  asm volatile("" : "+v"(tid_e));
+  const int q4e = (tid_e & 63) >> 4, l16e = tid_e & 15;
   if (p.ksplit > 1) {
     // Split K: the raw float32 sums go to part[ks][row][B row]; the reduce
     // kernel adds the splits in order and applies the epilogue.
     float* P = p.part + static_cast<int64_t>(ks) * p.M * p.part_ld;
 #pragma unroll
     for (int j = 0; j < JN; ++j) {
-      const int rr = brow[j];  // tile B row (output column) of this lane
+      const int rr = (EPI == kEpiSwiGLU ? wn * (WN / 2) : wn * WN) + l16e + bblk(j);  // tile B row (output column) of this lane
       int col;
       bool ok;
       if (EPI == kEpiSwiGLU) {
@@ -345,8 +367,8 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
 #pragma unroll
       for (int i = 0; i < IM; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WM + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + wm * WM + i * 16 + q4e * 4 + r;
           if (row < p.M) P[static_cast<int64_t>(row) * p.part_ld + col] = acc[i][j][r];
         }
     }
@@ -364,58 +386,60 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
     const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
         static_cast<float*>(p.C) + static_cast<int64_t>(m0s) * p.ldc, 0, c_bytes, 0x00020000);
     auto off = [&](int i, int r, int j) -> uint32_t {
-      const int row = wm * WM + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-      const int col = tn * BN + wn * WN + j * 32 + l32;
+      const int row = wm * WM + i * 16 + q4e * 4 + r;
+      const int col = tn * BN + wn * WN + j * 16 + l16e;
       return col < p.N ? static_cast<uint32_t>(row * p.ldc + col) * 4u : c_bytes;
     };
-    // Half blocks q = (block i = q / 2, rows 8 (q % 2) .. + 8) are double
-    // buffered (32 registers; whole blocks would take 64).
-    float cv[2][JN][8];  // [buffer][j][r]
-    auto load_half = [&](int q, float (*v)[8]) {
+    // Row blocks i are double buffered (2 x JN x 4 registers).
+    float cv[2][JN][4];  // [buffer][j][r]
+    auto load_block = [&](int i, float (*v)[4]) {
 #pragma unroll
-      for (int r = 0; r < 8; ++r)
+      for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int j = 0; j < JN; ++j)
-          v[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, off(q >> 1, (q & 1) * 8 + r, j), 0, 0));
+          v[j][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rc, off(i, r, j), 0, 0));
     };
-    load_half(0, cv[0]);
+    load_block(0, cv[0]);
 #pragma unroll
-    for (int q = 0; q < 2 * IM; ++q) {
-      if (q + 1 < 2 * IM) load_half(q + 1, cv[(q + 1) & 1]);
+    for (int i = 0; i < IM; ++i) {
+      if (i + 1 < IM) load_block(i + 1, cv[(i + 1) & 1]);
       // The sums go back into the accumulators and are stored from there:
       // a store reads its data register late, so storing from cv would make
-      // the loads of the next half block wait for these stores.  (The sum
-      // goes through a temporary: writing acc[i][j][r] and reading it back
-      // in the same unrolled loop was miscompiled by the ROCm 7.2 clang; a
+      // the loads of the next block wait for these stores.  (The sum goes
+      // through a temporary: writing acc[i][j][r] and reading it back in
+      // the same unrolled loop was miscompiled by the ROCm 7.2 clang; a
       // probe stored element 0's sum for every r.)
 #pragma unroll
-      for (int r = 0; r < 8; ++r)
+      for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int j = 0; j < JN; ++j) {
-          const int i = q >> 1, rr = (q & 1) * 8 + r;
-          const float sum = cv[q & 1][j][r] + acc[i][j][rr];
-          acc[i][j][rr] = sum;
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sum), rc, off(i, rr, j), 0, 0);
+          const float sum = cv[i & 1][j][r] + acc[i][j][r];
+          acc[i][j][r] = sum;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, sum), rc, off(i, r, j), 0, 0);
         }
     }
   } else {
 #pragma unroll
   for (int i = 0; i < IM; ++i) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm * WM + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + wm * WM + i * 16 + q4e * 4 + r;
       if (row >= p.M) continue;
       if (EPI == kEpiSwiGLU) {
+        // gate block j and up block j + JN/2 hold the same output columns
         uint16_t* C = static_cast<uint16_t*>(p.C) + static_cast<int64_t>(row) * p.ldc;
-        const int col = tn * (BN / 2) + wn * 32 + l32;
-        if (col < p.N) {
-          const float gt = acc[i][0][r], up = acc[i][1][r];
-          C[col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+#pragma unroll
+        for (int j = 0; j < JN / 2; ++j) {
+          const int col = tn * (BN / 2) + wn * (WN / 2) + j * 16 + l16e;
+          if (col < p.N) {
+            const float gt = acc[i][j][r], up = acc[i][j + JN / 2][r];
+            C[col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+          }
         }
       } else {
 #pragma unroll
         for (int j = 0; j < JN; ++j) {
-          const int col = tn * BN + wn * WN + j * 32 + l32;
+          const int col = tn * BN + wn * WN + j * 16 + l16e;
           if (col >= p.N) continue;
           if (EPI == kEpiF32) {
             float* C = static_cast<float*>(p.C) + static_cast<int64_t>(row) * p.ldc;
