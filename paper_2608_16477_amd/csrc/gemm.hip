@@ -34,11 +34,10 @@ namespace pallas {
 
 namespace {
 
-constexpr int BM = 256, BK = 64;
+constexpr int BK = 64;
 constexpr int KK = BK / 32;              // MFMA K-substeps per K-step
 constexpr int kThreads = 512;
 constexpr int kChunks = BK / 8;          // 16-byte chunks per tile row
-constexpr int kSlotsA = BM * kChunks;    // 16-byte slots of the A tile
 // Only waves 0-3 (one per SIMD) issue the operand loads: a wave blocked
 // on a full L1 miss queue cannot issue MFMAs, and this keeps waves 4-7
 // issuing MFMAs on every SIMD.
@@ -46,24 +45,36 @@ constexpr int kLoaderWaves = 4;
 constexpr int kXcds = 8;
 constexpr int kGroupM = 6;
 
-// Tile shapes: BN = 256 (8 waves as 2 x 4, each 128 x 64 = 8 x 4 blocks of
-// 16 x 16; a 2-deep LDS ring of 64 KiB stages) or BN = 128 (8 waves as 4 x
-// 2, each 64 x 64 = 4 x 4 blocks; a 3-deep ring of 48 KiB stages, since a
-// half-width step has half the MFMA work to hide its loads behind), for
-// launches whose 256-wide tiles would leave many CUs idle.  Both run the
+// Tile shapes BM x BN (output rows x B rows), all with 8 waves and the
 // same MFMA over the same K order, so an output element gets the same bits
-// from either.
-template <int BN_>
+// from any of them (a prefill's rows do not depend on its length):
+//   256 x 256: waves 2 x 4, each 128 x 64 (8 x 4 blocks of 16 x 16), a
+//              2-deep LDS ring of 64 KiB stages;
+//   256 x 128: waves 4 x 2, each 64 x 64; a 3-deep ring of 48 KiB stages,
+//              since a half-width step has half the MFMA work to hide its
+//              loads behind;
+//   192 x 256, 192 x 192, 192 x 128: waves 2 x 4, 2 x 4, 4 x 2, each 96 x 64,
+//              96 x 48, 48 x 64; 2, 3 and 4-deep rings (56, 48, 40 KiB
+//              stages; the smaller the tile, the less MFMA work a step
+//              has to hide its loads behind).
+// The 192-row shapes exist for row counts such as 1536 = 8 x 192, where
+// 256-row tiles leave CUs idle (gemm_tile).
+template <int BM_, int BN_>
 struct TileCfg {
-  static constexpr int BN = BN_;
-  static constexpr int kStages = BN_ == 256 ? 2 : 3;
-  static constexpr int WAVES_N = BN_ == 256 ? 4 : 2;
-  static constexpr int WM = BM / (8 / WAVES_N);   // rows per wave
-  static constexpr int WN = BN_ / WAVES_N;        // columns per wave (64)
+  static constexpr int BM = BM_, BN = BN_;
+  static constexpr int WAVES_N = BN_ == 128 ? 2 : 4;
+  static constexpr int WAVES_M = 8 / WAVES_N;
+  static constexpr int WM = BM_ / WAVES_M;        // rows per wave
+  static constexpr int WN = BN_ / WAVES_N;        // B rows (columns) per wave
   static constexpr int IM = WM / 16, JN = WN / 16;
-  static constexpr int kSlotsB = BN_ * kChunks;
+  static constexpr int kSlotsA = BM_ * kChunks, kSlotsB = BN_ * kChunks;   // 16-byte slots
+  static constexpr int kStageBytes = (kSlotsA + kSlotsB) * 16;
+  static constexpr int kStages = 4 * kStageBytes <= 160 * 1024 ? 4 : 3 * kStageBytes <= 150 * 1024 ? 3 : 2;
   static constexpr int kLoadsA = kSlotsA / (kLoaderWaves * 64);   // per loader thread
   static constexpr int kLoadsB = kSlotsB / (kLoaderWaves * 64);
+  static_assert(WM % 16 == 0 && WN % 16 == 0, "whole 16 x 16 blocks per wave");
+  static_assert(kLoadsA * kLoaderWaves * 64 == kSlotsA && kLoadsB * kLoaderWaves * 64 == kSlotsB,
+                "the loader waves fill the tiles exactly");
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -105,8 +116,9 @@ __device__ __forceinline__ void load_tile_lds(__amdgpu_buffer_rsrc_t rsrc, uint3
   for (int i = 0; i < N; ++i) load_row_lds<N, kTail>(rsrc, limit, voff, kcol, step, k0, K, lds_tile, wave, i);
 }
 
-template <int BN_>
-using LdsRing = u32x4[TileCfg<BN_>::kStages][kSlotsA + TileCfg<BN_>::kSlotsB];   // [stage][A slots, B slots]
+template <int BM_, int BN_>
+using LdsRing = u32x4[TileCfg<BM_, BN_>::kStages][TileCfg<BM_, BN_>::kSlotsA + TileCfg<BM_, BN_>::kSlotsB];
+// ([stage][A slots, B slots])
 
 // How a workgroup finds its work unit.  Workgroups are dealt round-robin
 // over the 8 XCDs; XCD x owns the contiguous run of units
@@ -118,10 +130,13 @@ enum { kUnitsPlain = 0, kUnitsTailFull = 1, kUnitsTailHalf = 2 };
 
 // One workgroup: its unit, then the output tile (M tile tm, column tile tn
 // of BN_ B rows) over its K split, with its LDS ring `lds`.
-template <int EPI, int BN_, int kUnits>
-__device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>& lds) {
-  using T = TileCfg<BN_>;
-  constexpr int BN = T::BN, IM = T::IM, JN = T::JN, WM = T::WM, WN = T::WN;
+template <int EPI, int BM_, int BN_, int kUnits>
+__device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BM_, BN_>& lds) {
+  using T = TileCfg<BM_, BN_>;
+  constexpr int BM = T::BM, BN = T::BN, IM = T::IM, JN = T::JN, WM = T::WM, WN = T::WN;
+  constexpr int kSlotsA = T::kSlotsA;
+  static_assert(EPI != kEpiSwiGLU || (JN % 2 == 0 && (BN / 2) % (8 * T::kLoadsB) == 0),
+                "SwiGLU: gate and up blocks pair up, and a loader wave's B rows stay in one half");
   constexpr int kLoadsA = T::kLoadsA, kLoadsB = T::kLoadsB;
   constexpr int kStages = T::kStages, kLoadsStep = kLoadsA + kLoadsB;
   unsigned long long c0 = 0, w0 = 0;
@@ -199,7 +214,6 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
     b_off[i] = static_cast<uint32_t>(gn * p.ldb * 2 + chunk * 16);
   }
   static_assert(kLoadsA % 2 == 0 && kLoadsB % 2 == 0, "loads come in even/odd pairs");
-  static_assert(BN / 2 % (8 * kLoadsB) == 0, "a wave's B rows stay in one half");
   const uint32_t a_step = 8u * p.lda * 2u, b_step = 8u * p.ldb * 2u;
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)p.A, 0, p.a_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)p.B, 0, p.b_bytes, 0x00020000);
@@ -236,7 +250,9 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
       }
     }
   }
-  if (kStages == 3 && KT > 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsStep) : "memory");
+  // Wait for step 0; up to kStages - 1 later steps stay in flight.
+  if (kStages == 4 && KT > 3) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * kLoadsStep) : "memory");
+  else if (kStages >= 3 && KT > 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsStep) : "memory");
   else if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoadsStep) : "memory");
   else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -264,14 +280,13 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
   }
   // One substep: the MFMAs on fa and bc, in groups of one A block (JN
   // MFMAs), each followed by that block's re-read for the next substep
-  // (substep kk of `slot`; its last use is just done), one of the next
-  // substep's B blocks into bn while any remain, and, in a loader wave's
-  // refill substep, kPer of its operand loads for K-step `kload` into
+  // (substep kk of `slot`; its last use is just done), the next
+  // substep's B blocks into bn (block i in group i, or JN / IM per group
+  // when there are more B than A blocks), and, in a loader wave's refill
+  // substep, an even share of its operand loads for K-step `kload` into
   // `lslot`.  A scheduling fence closes each group, so a block's re-read
   // cannot move above its MFMAs (which would need a second A buffer) and
   // the loads spread over the substep.
-  constexpr int kPer = kLoadsStep / IM;
-  static_assert(kPer * IM == kLoadsStep && JN <= IM, "loads and B reads spread over the A groups");
   auto substep = [&](const bf16x8* bc, int slot, int kk, bf16x8* bn, auto loads_tag, auto tail_tag, int kload,
                      int lslot) {
     constexpr bool kLoads = decltype(loads_tag)::value;
@@ -283,11 +298,16 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
 #pragma unroll
       for (int j = 0; j < JN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], bc[j], acc[i][j], 0, 0, 0);
-      if (i < JN) bn[i] = frag(Bb, bblk(i));
+      if constexpr (JN <= IM) {
+        if (i < JN) bn[i] = frag(Bb, bblk(i));
+      } else {
+#pragma unroll
+        for (int j = i * JN / IM; j < (i + 1) * JN / IM; ++j) bn[j] = frag(Bb, bblk(j));
+      }
       fa[i] = frag(Ab, i * 16);
       if constexpr (kLoads) {
 #pragma unroll
-        for (int q = i * kPer; q < (i + 1) * kPer; ++q) {
+        for (int q = i * kLoadsStep / IM; q < (i + 1) * kLoadsStep / IM; ++q) {
           if (q < kLoadsA)
             load_row_lds<kLoadsA, kTail>(ra, p.a_bytes, a_off, kcol_a, a_step, kload, p.K, lds[lslot], wave, q);
           else
@@ -309,7 +329,7 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
   auto step = [&](int kt, auto refill_tag, auto loader_tag, auto tail_tag) {
     constexpr bool kRefill = decltype(refill_tag)::value;
     constexpr bool kLoader = decltype(loader_tag)::value;
-    const int slot = kStages == 2 ? (kt & 1) : kt % kStages;
+    const int slot = kStages == 2 ? (kt & 1) : kStages == 4 ? (kt & 3) : kt % kStages;
     const int next = kStages == 2 ? (slot ^ 1) : (slot + 1 == kStages ? 0 : slot + 1);
     // Opaque to the optimiser each step, so the per-load offset sums stay
     // at the loads instead of being hoisted out of the loop.
@@ -317,7 +337,9 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
 #pragma unroll
     for (int kk = 0; kk < KK - 1; ++kk)
       substep(fb[kk & 1], slot, kk + 1, fb[(kk + 1) & 1], std::false_type{}, tail_tag, 0, 0);
-    if (kRefill && kStages == 3) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoadsStep) : "memory");
+    // Step kt+1 must have landed; steps kt+2 .. kt+kStages-1 may not have.
+    if (kRefill && kStages == 4) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsStep) : "memory");
+    else if (kRefill && kStages == 3) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kLoadsStep) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     // Step kt+1 is resident; its slot index is valid even past the end
@@ -462,10 +484,10 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BN_>
 }
 
 // Tiles of one width.
-template <int EPI, int BN_>
+template <int EPI, int BM_, int BN_>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) LdsRing<BN_> lds;
-  gemm_workgroup<EPI, BN_, kUnitsPlain>(p, lds);
+  __shared__ __attribute__((aligned(16))) LdsRing<BM_, BN_> lds;
+  gemm_workgroup<EPI, BM_, BN_, kUnitsPlain>(p, lds);
 }
 
 // Full-width tiles with a split tail: the last p.tail_half full tiles of
@@ -473,12 +495,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(GemmParams p) {
 // tiles each, so that round ends sooner.  Same bits as full-width tiles.
 template <int EPI>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_tail_kernel(GemmParams p) {
-  static_assert(sizeof(LdsRing<128>) >= sizeof(LdsRing<256>), "the half-width ring is the larger");
-  __shared__ __attribute__((aligned(16))) LdsRing<128> lds;
+  static_assert(sizeof(LdsRing<256, 128>) >= sizeof(LdsRing<256, 256>), "the half-width ring is the larger");
+  __shared__ __attribute__((aligned(16))) LdsRing<256, 128> lds;
   const int loc = static_cast<int>(blockIdx.x) / kXcds;
   if (loc >= p.tiles_per_xcd + p.tail_half) return;
-  if (loc >= p.tiles_per_xcd - p.tail_half) gemm_workgroup<EPI, 128, kUnitsTailHalf>(p, lds);
-  else gemm_workgroup<EPI, 256, kUnitsTailFull>(p, reinterpret_cast<LdsRing<256>&>(lds));
+  if (loc >= p.tiles_per_xcd - p.tail_half) gemm_workgroup<EPI, 256, 128, kUnitsTailHalf>(p, lds);
+  else gemm_workgroup<EPI, 256, 256, kUnitsTailFull>(p, reinterpret_cast<LdsRing<256, 256>&>(lds));
 }
 
 // Split-K reduction: C = epilogue(sum over ks of part[ks]), the splits
@@ -517,6 +539,25 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* __restric
   }
 }
 
+// The instantiation for a tile shape (gemm_tile never picks 192-wide B
+// tiles for the SwiGLU product, which has no such instantiation).
+template <int EPI>
+void launch_tiles(const GemmParams& p, int bm, int bn, int grid, hipStream_t s) {
+  if (bm == 256 && bn == 128) gemm_bf16_kernel<EPI, 256, 128><<<grid, kThreads, 0, s>>>(p);
+  else if (bm == 192 && bn == 256) gemm_bf16_kernel<EPI, 192, 256><<<grid, kThreads, 0, s>>>(p);
+  else if (bm == 192 && bn == 128) gemm_bf16_kernel<EPI, 192, 128><<<grid, kThreads, 0, s>>>(p);
+  else if constexpr (EPI != kEpiSwiGLU) {
+    if (bm == 192 && bn == 192) {
+      gemm_bf16_kernel<EPI, 192, 192><<<grid, kThreads, 0, s>>>(p);
+      return;
+    }
+  }
+  if (bm == 256 && bn == 256) {
+    if (p.tail_half) gemm_bf16_tail_kernel<EPI><<<grid, kThreads, 0, s>>>(p);
+    else gemm_bf16_kernel<EPI, 256, 256><<<grid, kThreads, 0, s>>>(p);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, int ldb, void* C,
@@ -537,9 +578,10 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   p.lda = lda;
   p.ldb = ldb;
   p.ldc = ldc;
-  p.tiles_m = (M + BM - 1) / BM;
   p.ksplit = gemm_ksplit(epi, M, N, K);
-  const int bn = p.ksplit == 1 ? gemm_tile_bn(epi, M, N) : 256;
+  const GemmTile tile = p.ksplit == 1 ? gemm_tile(epi, M, N) : GemmTile{256, 256};
+  const int bm = tile.bm, bn = tile.bn;
+  p.tiles_m = (M + bm - 1) / bm;
   p.tiles_n = gemm_tiles_n(epi, N, bn);
   p.total_tiles = p.tiles_m * p.tiles_n;
   p.part = part;
@@ -552,7 +594,7 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   // A last round that keeps at most half of an XCD's 32 CUs busy runs as
   // half-width tiles (full-width launches without a K split only).
   p.tail_half = 0;
-  if (bn == 256 && p.ksplit == 1) {
+  if (bm == 256 && bn == 256 && p.ksplit == 1) {
     const int rounds = (p.tiles_per_xcd + 31) / 32, last = p.tiles_per_xcd - 32 * (rounds - 1);
     if (rounds > 1 && last <= 16) p.tail_half = last;
   }
@@ -562,20 +604,13 @@ hipError_t launch_gemm(int epi, const uint16_t* A, int lda, const uint16_t* B, i
   p.b_bytes = static_cast<uint32_t>(brows * ldb * 2);
   p.clk = clk;
   const int grid = (p.tiles_per_xcd + p.tail_half) * kXcds;
-#define PALLAS_GEMM_LAUNCH(E)                                                   \
-  case E:                                                                       \
-    if (bn == 128) gemm_bf16_kernel<E, 128><<<grid, kThreads, 0, s>>>(p);       \
-    else if (p.tail_half) gemm_bf16_tail_kernel<E><<<grid, kThreads, 0, s>>>(p);\
-    else gemm_bf16_kernel<E, 256><<<grid, kThreads, 0, s>>>(p);                 \
-    break;
   switch (epi) {
-    PALLAS_GEMM_LAUNCH(kEpiBf16)
-    PALLAS_GEMM_LAUNCH(kEpiAddF32)
-    PALLAS_GEMM_LAUNCH(kEpiSwiGLU)
-    PALLAS_GEMM_LAUNCH(kEpiF32)
+    case kEpiBf16: launch_tiles<kEpiBf16>(p, bm, bn, grid, s); break;
+    case kEpiAddF32: launch_tiles<kEpiAddF32>(p, bm, bn, grid, s); break;
+    case kEpiSwiGLU: launch_tiles<kEpiSwiGLU>(p, bm, bn, grid, s); break;
+    case kEpiF32: launch_tiles<kEpiF32>(p, bm, bn, grid, s); break;
     default: return hipErrorInvalidValue;
   }
-#undef PALLAS_GEMM_LAUNCH
   if (p.ksplit > 1) {
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
     const int64_t threads = int64_t(M) * (N / 4);

@@ -64,21 +64,45 @@ struct GemmParams {
   unsigned long long* clk;
 };
 
-// Output-column tiles of one 256-row M tile, for tiles of bn B rows
-// (gate|up: bn/2 gate + bn/2 up rows, so bn/2 output columns per tile).
+// Output-column tiles for tiles of bn B rows (gate|up: bn/2 gate + bn/2
+// up rows, so bn/2 output columns per tile).
 inline int gemm_tiles_n(int epi, int N, int bn = 256) {
   const int cols = epi == kEpiSwiGLU ? bn / 2 : bn;
   return (N + cols - 1) / cols;
 }
-// B rows per tile: 256, or 128 when 256-row tiles would leave so many of
-// the 256 CUs idle that half-width tiles finish in at most three quarters
-// of the rounds (the mid model's O and down projections at 1536 rows: 96
-// tiles).  The tile width does not change any output bit.
-inline int gemm_tile_bn(int epi, int M, int N) {
-  const int tm = (M + 255) / 256;
-  const int t256 = tm * gemm_tiles_n(epi, N, 256), t128 = tm * gemm_tiles_n(epi, N, 128);
-  const int r256 = (t256 + 255) / 256, r128_x2 = (t128 + 255) / 256;   // rounds of full / half tiles
-  return 4 * r128_x2 <= 6 * r256 ? 128 : 256;                           // 0.5 r128 <= 0.75 r256
+// Tile shape (output rows bm x B rows bn) of a launch without a K split.
+// Every shape runs the same MFMA over the same K order, so the choice never
+// changes an output bit.  A launch takes rounds of one workgroup per CU,
+// dealt to the 8 XCDs' 32 CUs each; its time is modelled as rounds x tile
+// area / the shape's FLOP rate per CU relative to 256 x 256, measured at
+// the large and mid shapes (a 256 x 256 launch whose last round keeps at
+// most half the CUs busy runs that round as half-width tiles, at
+// 0.5 / 0.77 of a round).  The 192-row shapes fit row counts such as
+// 1536 = 8 x 192 (the mid model: Q|K|V 144 tiles of 256 x 256 but 256 of
+// 192 x 192; O and down 96 but 256 of 192 x 128).
+struct GemmTile {
+  int bm, bn;
+};
+inline GemmTile gemm_tile(int epi, int M, int N) {
+  struct Cand {
+    int bm, bn, rate;   // rate: FLOP rate per CU, percent of 256 x 256
+  };
+  static const Cand cands[] = {{256, 256, 100}, {256, 128, 77}, {192, 256, 85}, {192, 192, 80}, {192, 128, 70}};
+  GemmTile best{256, 256};
+  double best_cost = 0;
+  for (const Cand& c : cands) {
+    if (epi == kEpiSwiGLU && c.bn == 192) continue;   // gate and up blocks pair up
+    const int tiles = ((M + c.bm - 1) / c.bm) * gemm_tiles_n(epi, N, c.bn);
+    const int per_xcd = (tiles + 7) / 8, rounds = (per_xcd + 31) / 32;
+    double r = rounds;
+    if (c.bm == 256 && c.bn == 256 && rounds > 1 && per_xcd - 32 * (rounds - 1) <= 16) r = rounds - 1 + 0.5 / 0.77;
+    const double cost = r * c.bm * c.bn / c.rate;
+    if (best_cost == 0 || cost < best_cost) {
+      best = {c.bm, c.bn};
+      best_cost = cost;
+    }
+  }
+  return best;
 }
 
 // K-range splits per tile.  Only GEMMs of a single 256-row M tile split

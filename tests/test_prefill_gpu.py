@@ -192,7 +192,8 @@ def test_profile_clock_samples_gemm_launches(P):
         P.pallas_profile_enable([])
         P.pallas_profile_reset()
     # 2 M tiles x 6 gate|up column groups of 128 would fill 12 of 256 CUs,
-    # so the launch runs half-width tiles: 2 x 11 groups of 64 columns.
-    tiles = -(-300 // 256) * -(-cfg.ffn // 64)
+    # so the launch runs the smallest tiles: 2 x 192 rows x 11 groups of 64
+    # columns.
+    tiles = -(-300 // 192) * -(-cfg.ffn // 64)
     assert wgs == tiles * (cfg.n_layers - 1)
     assert 0.3 < ghz < 3.5
