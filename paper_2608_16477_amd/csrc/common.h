@@ -39,6 +39,14 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
+// SwiGLU of one output: silu(gate) * up, silu(g) = g / (1 + e^-g), the
+// division taken as a multiply by the hardware reciprocal (v_rcp_f32,
+// within 1 ulp): the IEEE division sequence costs a dozen instructions per
+// output in the GEMM epilogues, and the result is rounded to bf16.
+__device__ __forceinline__ float swiglu(float gate, float up) {
+  return gate * __builtin_amdgcn_rcpf(1.0f + __expf(-gate)) * up;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

@@ -456,7 +456,7 @@ __device__ __forceinline__ void gemm_workgroup(const GemmParams& p, LdsRing<BM_,
           const int col = tn * (BN / 2) + wn * (WN / 2) + j * 16 + l16e;
           if (col < p.N) {
             const float gt = acc[i][j][r], up = acc[i][j + JN / 2][r];
-            C[col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+            C[col] = f2bf(swiglu(gt, up));
           }
         }
       } else {
@@ -531,7 +531,7 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(const float* __restric
   } else {
     if (EPI == kEpiSwiGLU) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) a[e] = a[e] / (1.0f + __expf(-a[e])) * up[e];
+      for (int e = 0; e < 4; ++e) a[e] = swiglu(a[e], up[e]);
     }
     u32x2 w;
     w.x = pack_bf2(a[0], a[1]);

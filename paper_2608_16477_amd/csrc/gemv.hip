@@ -226,7 +226,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const uint16_t* __restri
       const int col = tile * 16 + li;
       if (col < N) {
         const float gt = sum[0][r], up = sum[TILES - 1][r];
-        static_cast<uint16_t*>(C)[static_cast<int64_t>(m) * ldc + col] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+        static_cast<uint16_t*>(C)[static_cast<int64_t>(m) * ldc + col] = f2bf(swiglu(gt, up));
       }
     } else {
 #pragma unroll
