@@ -47,9 +47,9 @@ NOMINAL_SCLK_GHZ = 2.4      # clock the MFMA peak is quoted at
 # only for the GEMM source it was measured on: a different csrc/gemm.hip
 # reports null.
 GEMM_TRAFFIC = {
-    "gemm_source_sha256_16": "3b69242dede6a89d",
-    "fetch_kib": 1.33508e6, "fetch_scale": 2.0,
-    "write_kib": 2.07834e5, "write_scale": 1.0,
+    "gemm_source_sha256_16": "02fe53aa9dc84ac5",
+    "fetch_kib": 1.34892e6, "fetch_scale": 2.0,
+    "write_kib": 1.94010e5, "write_scale": 1.0,
 }
 
 
