@@ -270,15 +270,6 @@ __global__ __launch_bounds__(G * 64, G == 4 ? 2 : 1) void attn_prefill_kernel(At
         const bf16x8 a = __builtin_bit_cast(bf16x8, Kb[kk * 2 * KSTR + t * 32]);
         st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], kk == 0 ? f32x16{} : st[t], 0, 0, 0);
       }
-    // Keep eight K-fragment reads in flight ahead of the MFMAs.
-#pragma unroll
-    for (int i = 0; i < 8; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-#pragma unroll
-    for (int i = 0; i < D / 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      if (i + 8 < D / 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-    }
   };
 
   f32x16 oacc[D / 32];
