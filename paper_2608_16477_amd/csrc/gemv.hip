@@ -254,19 +254,23 @@ int gemv_ksplit(int epi, int N, int K) {
   // Workgroups per tile, for launches of fewer than two tiles per CU (O and
   // down at the large shape: 320 tiles): the split whose workgroup count
   // divides most evenly over the 256 CUs, with at least four 64-wide
-  // K-steps per wave, and only when it beats no split by more than 5%.
-  // Measured at the large shape, M = 1: O 21.6 -> 18.8 us and down 64 ->
-  // 58 us with four splits; Q|K|V (640 tiles) and gate|up (1600) ran 10%
-  // slower split in two, so they do not split.
+  // K-steps per wave and every workgroup resident at once (the LDS stages
+  // hold four single-tile or two gate|up workgroups per CU), and only when it beats no
+  // split by more than 5%.  Measured at the large shape, M = 1: O 21.6 ->
+  // 18.8 us and down 64 -> 58 us with four splits, and three (960
+  // workgroups) beat four (1280, a fifth of them in a second round): the
+  // decode step 14.94 -> 14.63 ms.  Q|K|V (640 tiles) and gate|up (1600)
+  // ran 10% slower split in two, so they do not split.
   const int tiles = (N + 15) / 16;
   if (tiles >= 512) return 1;
+  const int resident = 256 * (epi == kEpiSwiGLU ? 2 : 4);
   auto eff = [&](int s) {
     const double per_cu = double(tiles) * s / 256.0;
     return per_cu / std::ceil(per_cu);
   };
   int best = 1;
   for (int s = 2; s <= kGemvMaxSplit; ++s) {
-    if (K / (s * kWaves * kKStep) < 4) break;
+    if (K / (s * kWaves * kKStep) < 4 || tiles * s > resident) break;
     if (eff(s) > eff(best) + 0.05) best = s;
   }
   return best;

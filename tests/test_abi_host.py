@@ -319,7 +319,9 @@ def test_static_decode_host_rejections(P):
     its own limits, all before it touches the device: more than
     PALLAS_STATIC_DECODE_MAX_SEQS (8) sequences, or a step whose scratch
     need exceeds PALLAS_STATIC_SCRATCH_BYTES (64 MiB): 8 sequences at
-    position 15,680 of the 64-layer shape need 64.02 MiB.  (A call that
+    position 15,744 of the large shape need 64.22 MiB (at 15,743, 63.97
+    MiB: the decode-attention records grow by one 64-key split there).
+    (A call that
     passes every check is not made here: with a device present it would
     launch kernels on the fake pointers.)"""
     from workloads import configs
@@ -336,7 +338,7 @@ def test_static_decode_host_rejections(P):
         assert rc([16384]) == P.Status.UNSUPPORTED
         assert rc([5] * 9) == P.Status.UNSUPPORTED
         assert "at most 8" in P.pallas_last_error()
-        assert rc([15680] * 8) == P.Status.UNSUPPORTED
+        assert rc([15744] * 8) == P.Status.UNSUPPORTED
         assert "scratch" in P.pallas_last_error()
         assert rc([-1]) == P.Status.OUT_OF_RANGE
     finally:
