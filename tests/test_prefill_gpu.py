@@ -103,6 +103,44 @@ def test_layer_shapes_reduced_depth(P, shape):
     check_against_oracle(cfg, glob, layers, ids, pool, bt)
 
 
+# The large model's attention shape (64 query heads over 8 KV heads,
+# head_dim 128, QK-norm) with a narrower residual stream and FFN, so the
+# oracle stays cheap; the projections still split K at 256 rows and below.
+LARGE_HEADS = configs.LARGE.replace(n_layers=2, vocab=4096, hidden=1024, ffn=4096, name="large-heads-L2")
+
+
+@pytest.mark.parametrize("p", [31, 32, 33, 64, 65, 256, 257])
+def test_large_heads_boundary_lengths(P, p):
+    """Prefixes around a 32-query block, a 64-key tile and the 256-row limit
+    of the split-K projections and attention key splits (256 splits, 257
+    does not)."""
+    cfg = LARGE_HEADS
+    glob, layers = gen.model_weights(cfg, seed=13, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    ids = gen.token_ids(p, cfg.vocab, seed=13, stream=p).numpy()
+    pages = (p + 15) // 16
+    bt = gen.block_table(pages, pages + 4, pages, 13, p)
+    pool = run_prefill(P, model, cfg, [ids], [bt], pages + 4)
+    check_against_oracle(cfg, glob, layers, ids, pool, bt)
+
+
+def test_large_heads_varlen_batch(P):
+    """Five sequences in one call with 66 query blocks x 8 KV heads (528
+    pairs): the undivided 8-head workgroups and the longest-first order
+    across sequences, sequences of one token and of block and tile edges."""
+    cfg = LARGE_HEADS
+    glob, layers = gen.model_weights(cfg, seed=14, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    lens = [1200, 1, 700, 65, 33]
+    assert sum((n + 31) // 32 for n in lens) * cfg.n_kv_heads >= 512
+    ids_list = [gen.token_ids(n, cfg.vocab, seed=14, stream=i).numpy() for i, n in enumerate(lens)]
+    pages = [(n + 15) // 16 for n in lens]
+    tables = gen.disjoint_block_tables(pages, 140, 80, 14, 5)
+    pool = run_prefill(P, model, cfg, ids_list, list(tables), 140)
+    for ids, bt in zip(ids_list, tables):
+        check_against_oracle(cfg, glob, layers, ids, pool, bt)
+
+
 def test_varlen_batch(P):
     cfg = configs.MID.replace(n_layers=2, vocab=4096, name="mid-L2")
     glob, layers = gen.model_weights(cfg, seed=2, gain_sigma=0.1)
