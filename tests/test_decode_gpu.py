@@ -1,11 +1,13 @@
 """GPU parity of the decode step at the large decoder's layer shape (2
 layers, hidden 5120, 64/8 heads, ffn 25600) against the oracle's decode over
 the oracle's cache: one sequence and a batch of three, logits within
-max|gpu - ref| <= 1e-2 max|ref| per row.  At this shape the skinny
-projections split K over workgroups (Q|K|V and gate|up two ways, O and down
-four ways) and reduce the partial sums in the last workgroup of each tile;
-two identical calls give identical logits.  Also a token decoding at
-position 0 (an empty cache) in one batch with another sequence."""
+max|gpu - ref| <= 1e-2 max|ref| per row.  At this shape the O and down
+projections split K three ways over workgroups and reduce the partial sums
+in the last workgroup of each tile (Q|K|V, gate|up and lm_head stream whole
+tiles); two identical calls give identical logits.  Also a token decoding
+at position 0 (an empty cache) in one batch with another sequence, and a
+batch of eight at the large attention shape whose positions span the
+decode attention's key splits."""
 import numpy as np
 import pytest
 import torch
@@ -101,3 +103,41 @@ def test_decode_at_position_zero_in_a_batch(P):
         for l in range(cfg.n_layers):
             assert rel_err(lv[l, 0, n], k_new[l][0]) <= TOL
             assert rel_err(lv[l, 1, n], v_new[l][0]) <= TOL
+
+
+def test_decode_large_heads_batch_of_eight(P):
+    """Eight sequences decoding in one call at the large model's attention
+    shape (64 query heads over 8 KV heads, head_dim 128, QK-norm; a narrower
+    residual stream and FFN keep the oracle cheap), at positions 0 (empty
+    cache), 1, 63, 64, 65 (one and two 64-key splits), 200, 1023 and 1100
+    (16 and 18 splits: the combine reads its records in batches of 16)."""
+    cfg = configs.LARGE.replace(n_layers=2, vocab=4096, hidden=1024, ffn=4096, name="large-heads-L2")
+    glob, layers = gen.model_weights(cfg, seed=33, gain_sigma=0.1)
+    model = gpu_model(P, cfg, glob, layers)
+    lens = [0, 1, 63, 64, 65, 200, 1023, 1100]
+    ids = [gen.token_ids(n + 1, cfg.vocab, seed=33, stream=i).numpy() for i, n in enumerate(lens)]
+    pages = [(n + 1 + 15) // 16 for n in lens]
+    tables = gen.disjoint_block_tables(pages, 200, 70, 33, 1)
+    d_bt = torch.tensor(tables, dtype=torch.int32, device=DEV)
+    pool = empty_pool(cfg, 200, fill_bits=0)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ws = model.workspace(max(lens), 8)
+    for i, n in enumerate(lens):
+        if n:
+            model.prefill_prefix(torch.tensor(ids[i][:n], dtype=torch.int32, device=DEV), [0, n], d_bt[i:i + 1],
+                                 pool, ws, err)
+    toks = torch.tensor([x[n] for x, n in zip(ids, lens)], dtype=torch.int32, device=DEV)
+    logits = torch.empty((8, cfg.vocab), dtype=torch.float32, device=DEV)
+    model.decode_step(toks, lens, d_bt, pool, logits, ws, err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    g, ls = oracle_weights(glob, layers)
+    shp = shape_of(cfg)
+    for i, n in enumerate(lens):
+        if n:
+            K, V, _ = om.prefill(list(ids[i][:n]), g, ls, shp)
+        else:
+            K = V = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(cfg.n_layers)]
+        ref, _, _ = om.decode(int(ids[i][n]), n, K, V, g, ls, shp)
+        e = rel_err(logits[i].cpu().double().numpy(), ref)
+        assert e <= TOL, f"sequence {i} at position {n}: logits rel err {e:.3g}"
