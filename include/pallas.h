@@ -304,7 +304,7 @@ int pallas_decode_step(pallas_model* m, int32_t num_seqs, const int32_t* d_token
  * PALLAS_STATIC_DECODE_MAX_SEQS sequences, and a scratch need within the
  * array: roughly num_seqs * n_q_heads * (max n_i / 64 + 1) * (head_dim + 2)
  * * 4 bytes of attention records plus the step's activations (at 64 query
- * heads of 128 and ffn 25600: 8 sequences up to position 15,679; fewer
+ * heads of 128 and ffn 25600: 8 sequences up to position 15,743; fewer
  * up to 16,383).
  * HIP on a failed device query. */
 #define PALLAS_STATIC_SCRATCH_BYTES (64u << 20)
