@@ -4,9 +4,9 @@
 // KV head) with one wave per query head, so each 64-key K/V tile is read
 // from the pool once for the G heads.  G is the GQA group, except that in
 // calls with too few query blocks to fill the chip a group of 8 at head_dim
-// 128 is split over two 4-wave workgroups, two of which fit on a CU (255
-// registers, 75 KB of LDS each).  K tiles go from memory straight into LDS (buffer_load ... lds);
-// V tiles are staged through registers and written transposed.
+// 128 is split over two 4-wave workgroups, two of which fit on a CU (under
+// 224 registers, 74 KB of LDS each).  K and V tiles go from memory straight
+// into LDS (buffer_load ... lds); V is read transposed for the PV product.
 //
 // The score tile is computed transposed, S^T = K Q^T, with
 // v_mfma_f32_32x32x16_bf16: a lane then owns one query and
