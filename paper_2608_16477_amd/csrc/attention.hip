@@ -565,11 +565,9 @@ __global__ __launch_bounds__(kDecThreads) void attn_decode_split_kernel(AttnPara
         }
       }
     }
+    static_assert(TPK == 4, "a key's score threads are one quad");
 #pragma unroll
-    for (int g = 0; g < kMaxG; ++g) {
-#pragma unroll
-      for (int o = 1; o < TPK; o <<= 1) acc[g] += __shfl_xor(acc[g], o, kWave);
-    }
+    for (int g = 0; g < kMaxG; ++g) acc[g] = quad_sum(acc[g]);
     if (qt == 0) {
       const bool valid = kok[key] != 0;
 #pragma unroll

@@ -47,15 +47,60 @@ __device__ __forceinline__ float swiglu(float gate, float up) {
   return gate * __builtin_amdgcn_rcpf(1.0f + __expf(-gate)) * up;
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+// Butterfly reductions over lane distances 32, 16, 8, 4, 2, 1 (in that
+// order), done with register lane exchanges instead of LDS permutes.  Each
+// step adds (or takes the max of) the values of lanes i and i ^ m, in one
+// operand order or the other, which is exact either way, so the results
+// are those of the __shfl_xor butterfly bit for bit:
+//   32, 16: v_permlane32_swap / v_permlane16_swap of a value with itself
+//           return the pair (v[i], v[i ^ m]) in some order;
+//   8:      DPP row_ror:8 reads lane (i + 8) mod 16 = i ^ 8 of the row;
+//   4:      DPP row_ror:4 reads lane i ^ 4 or i ^ 4 ^ 8, equal after the
+//           8-step;
+//   2, 1:   DPP quad permutes [2, 3, 0, 1] and [1, 0, 3, 2].
+template <int CTRL>
+__device__ __forceinline__ float dpp_read(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;    // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;    // quad_perm [2, 3, 0, 1]
+constexpr int kDppRor4 = 0x124;   // row_ror:4
+constexpr int kDppRor8 = 0x128;   // row_ror:8
+
+// Sum of the 4 lanes of a quad (distances 1, 2).
+__device__ __forceinline__ float quad_sum(float v) {
+  v += dpp_read<kDppXor1>(v);
+  v += dpp_read<kDppXor2>(v);
   return v;
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+// Sum of a 16-lane row (distances 8, 4, 2, 1).
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_read<kDppRor8>(v);
+  v += dpp_read<kDppRor4>(v);
+  v += dpp_read<kDppXor2>(v);
+  v += dpp_read<kDppXor1>(v);
   return v;
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_read<kDppRor8>(v));
+  v = fmaxf(v, dpp_read<kDppRor4>(v));
+  v = fmaxf(v, dpp_read<kDppXor2>(v));
+  v = fmaxf(v, dpp_read<kDppXor1>(v));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  return row16_sum(v);
+}
+__device__ __forceinline__ float wave_max(float v) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return row16_max(v);
 }
 
 }  // namespace pallas

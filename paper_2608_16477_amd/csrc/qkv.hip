@@ -72,8 +72,12 @@ __global__ __launch_bounds__(kThreads) void qkv_rope_kernel(QkvParams p, RowMap 
         float ss = 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) ss += x0[e] * x0[e] + x1[e] * x1[e];
+        if constexpr (LPH == 16) {
+          ss = row16_sum(ss);
+        } else {
 #pragma unroll
-        for (int o = LPH / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
+          for (int o = LPH / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
+        }
         const float inv = rsqrtf(ss / D + p.eps);
         const uint16_t* gsrc = is_q ? p.q_gain : p.k_gain;
         const u32x2 g0 = *reinterpret_cast<const u32x2*>(gsrc + 4 * j);
