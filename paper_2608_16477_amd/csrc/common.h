@@ -58,6 +58,9 @@ __device__ __forceinline__ float swiglu(float gate, float up) {
 //   4:      DPP row_ror:4 reads lane i ^ 4 or i ^ 4 ^ 8, equal after the
 //           8-step;
 //   2, 1:   DPP quad permutes [2, 3, 0, 1] and [1, 0, 3, 2].
+// Every lane of the group being reduced (the quad, the 16-lane row, the
+// wave) must be active: a DPP read from an inactive lane does not return
+// that lane's value.
 template <int CTRL>
 __device__ __forceinline__ float dpp_read(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
